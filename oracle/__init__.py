@@ -1,0 +1,57 @@
+"""CPU oracle for chunk-wise block-sparse causal attention over a streaming KV cache.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path may import, call or link
+anything in this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.
+
+It is a plain, slow, obviously correct restatement of what the method computes
+(Ultra Flash, arXiv 2606.09150):
+
+* ``ring``      -- the KV cache window of earlier chunks plus the current chunk
+                   (Sec. 2.3.2, dynamic cache management (iii), "SR cache length
+                   adaptation"; App. C, "KV cache: 3 temporal windows"), with a
+                   pinned first ("sink") chunk and oldest-first eviction.
+* ``keep``      -- the per-(head, query tile) key-tile keep set: the temporal
+                   causal mask of Sec. 2.3.1(a) intersected with a seeded
+                   Bernoulli content stand-in for the top-k rule of Eq. 4.
+                   The Bernoulli rule and its SplitMix64 counter hash are not in
+                   the paper: their parity against the paper is unpinned; they
+                   are pinned to the published SplitMix64 outputs and to
+                   binomial statistics.
+* ``attention`` -- softmax attention of the current chunk's queries over the
+                   union of kept key tiles (Eq. 4 mask semantics), computed as
+                   masked dense attention in float64.
+
+It shares no code with the HIP path (``paper_2606_09150_amd``) and imports
+nothing from it.
+"""
+
+from .ring import RingModel, RingCapacityError, RingEmptyError
+from .keep import (
+    KeepRule,
+    splitmix64,
+    keep_threshold,
+    tile_geometry,
+    keep_bits,
+    lists_from_bits,
+)
+from .attention import (
+    sparse_causal_attention,
+    sparse_causal_attention_rows,
+    dense_keys,
+)
+
+__all__ = [
+    "RingModel",
+    "RingCapacityError",
+    "RingEmptyError",
+    "KeepRule",
+    "splitmix64",
+    "keep_threshold",
+    "tile_geometry",
+    "keep_bits",
+    "lists_from_bits",
+    "sparse_causal_attention",
+    "sparse_causal_attention_rows",
+    "dense_keys",
+]
