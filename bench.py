@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark of the block-sparse chunk-causal attention path on one MI355X.
+
+One step = one chunk through the whole path, as a streaming SR DiT layer
+would run it: evict the oldest non-pinned chunk (once the window is full),
+append the new chunk's K and V, build the keep lists, run the attention of
+the new chunk's queries.  Inputs are seeded synthetic N(0,1) bf16 tensors
+already resident in HBM (a small rotating set of chunks); the keep lists
+change every step because they are keyed on the current chunk's sequence
+number.
+
+Prints ONE JSON line.  ``value`` is kept-tile TFLOP/s over the whole step
+(512 flop per kept, valid (query, key) pair: 4*D with D = 128), ``ms_per_step``
+is milliseconds per chunk.  ``roofline`` prices the attention kernel alone
+(its average duration from HIP events on the launch stream) against the bf16
+dense MFMA peak.  ``cpu_baseline`` times the CPU oracle on a bounded sample of
+the same workload on this host.
+
+    python bench.py [--steps K] [--warmup W] [--config 1k] [--secondary 2k]
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ms per chunk + effective TFLOP/s (kept tiles) of sparse causal attn, 1K & 2K"
+MFMA_BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
+HBM_PEAK_GBPS = 8000.0
+D = 128
+
+
+def _flops_of_lists(win, lists, nt, tail, T):
+    """Kept-tile FLOPs of one list buffer: 4*D per kept valid (query, key) pair."""
+    import torch
+    counts, idx, _ = win.lists_views(lists)
+    valid_k = torch.where(idx % nt == nt - 1, tail, T).to(torch.int64)
+    valid_k = torch.where(idx >= 0, valid_k, torch.zeros_like(valid_k)).sum(-1)      # [B,H,NT]
+    valid_q = torch.full((nt,), T, dtype=torch.int64, device=idx.device)
+    valid_q[-1] = tail
+    kept = int((valid_k * valid_q).sum().item()) * 4 * D
+    padded = int(counts.to(torch.int64).sum().item()) * T * T * 4 * D
+    return kept, padded
+
+
+def run_workload(P, wl, steps, warmup, n_src=3):
+    import torch
+    import synth
+
+    dev = torch.device("cuda", 0)
+    B, L, H, T = wl.batch, wl.chunk_tokens, wl.heads, wl.tile
+    nt = -(-L // T)
+    tail = L - (nt - 1) * T
+    win = P.KVWindow(B, H, L, T, wl.max_chunks, wl.pin_sink, device=dev)
+    srcs = [{name: synth.chunk_tensor(wl, c, name, device="cuda") for name in ("k", "v", "q")}
+            for c in range(n_src)]
+    # window up to (but excluding) the current chunk
+    for c in range(wl.window_chunks - 1):
+        win.append(srcs[c % n_src]["k"], srcs[c % n_src]["v"])
+    total = warmup + steps
+    lists = [torch.empty(win.layout.total_bytes, dtype=torch.uint8, device=dev) for _ in range(total)]
+    out = torch.empty((B, L, H, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
+    scale = 1.0 / math.sqrt(D)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(s):
+        src = srcs[(wl.window_chunks - 1 + s) % n_src]
+        if win.info().n_live == wl.max_chunks:
+            win.evict(1)
+        e = ev[s]
+        e[0].record(stream)
+        win.append(src["k"], src["v"])
+        e[1].record(stream)
+        win.lists = lists[s]
+        win.build_lists(wl.seed, wl.p_prior)
+        e[2].record(stream)
+        win.attention(src["q"], scale, out=out, lse=lse)
+        e[3].record(stream)
+
+    for s in range(warmup):
+        step(s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(warmup, total):
+        step(s)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / steps
+
+    append_ms = [ev[s][0].elapsed_time(ev[s][1]) for s in range(warmup, total)]
+    lists_ms = [ev[s][1].elapsed_time(ev[s][2]) for s in range(warmup, total)]
+    attn_ms = [ev[s][2].elapsed_time(ev[s][3]) for s in range(warmup, total)]
+    fl = [_flops_of_lists(win, lists[s], nt, tail, T) for s in range(warmup, total)]
+    kept = sum(f[0] for f in fl) / steps
+    padded = sum(f[1] for f in fl) / steps
+    dense = 4 * D * B * H * L * (L * wl.window_chunks)
+    attn_avg = sum(attn_ms) / steps
+    attn_sorted = sorted(attn_ms)
+    append_bytes = 2 * B * L * H * D * 2 + 2 * B * nt * T * H * D * 2
+    res = {
+        "workload": wl.name,
+        "ms_per_step": ms_step,
+        "value": kept / (ms_step * 1e-3) / 1e12,
+        "attn_ms": attn_avg,
+        "attn_ms_p10": attn_sorted[len(attn_sorted) // 10],
+        "attn_ms_p90": attn_sorted[(9 * len(attn_sorted)) // 10],
+        "attn_tflops": kept / (attn_avg * 1e-3) / 1e12,
+        "append_us": sum(append_ms) / steps * 1e3,
+        "append_gbps": append_bytes / (sum(append_ms) / steps * 1e-3) / 1e9,
+        "lists_us": sum(lists_ms) / steps * 1e3,
+        "kept_tflop_per_step": kept / 1e12,
+        "kept_fraction": kept / dense,
+        "padded_tile_tflop_per_step": padded / 1e12,
+        "keys": L * wl.window_chunks,
+    }
+    state = {"win": win, "srcs": srcs, "n_src": n_src, "steps_done": total}
+    return res, state
+
+
+def cpu_baseline(wl, state, target_s):
+    """The oracle, as it stands, on a bounded sample: head 0 of the last window, leading q-tiles."""
+    import numpy as np
+
+    import oracle
+
+    win = state["win"]
+    srcs, n_src = state["srcs"], state["n_src"]
+    B, L, H, T = wl.batch, wl.chunk_tokens, wl.heads, wl.tile
+    nt = -(-L // T)
+    tail = L - (nt - 1) * T
+    info = win.info()
+    seqs = [win.logical(p)[1] for p in range(info.n_live)]
+    # chunk with sequence number s was appended from srcs[s % n_src]
+    ring = oracle.RingModel(wl.max_chunks, wl.pin_sink)
+    meta = oracle.RingModel(wl.max_chunks, wl.pin_sink)
+    zeros = np.broadcast_to(np.zeros(1), (B, L, H, 1))
+    for s in range(seqs[-1] + 1):
+        if s in seqs:
+            src = srcs[s % n_src]
+            ring.live.append(oracle.ring.Chunk(s, wl.pin_sink and s == 0,
+                                               src["k"][:, :, 0:1].double().cpu().numpy(),
+                                               src["v"][:, :, 0:1].double().cpu().numpy()))
+            meta.live.append(oracle.ring.Chunk(s, wl.pin_sink and s == 0, zeros, None))
+    q = srcs[seqs[-1] % n_src]["q"][:, :, 0:1].double().cpu().numpy()
+    bits = oracle.keep_bits(meta, T, oracle.KeepRule(wl.seed, wl.p_prior))[:, 0:1]
+    scale = 1.0 / math.sqrt(D)
+
+    def kept_flops(tiles):
+        f = 0
+        for i in tiles:
+            vq = tail if i == nt - 1 else T
+            for j in np.nonzero(bits[0, 0, i])[0]:
+                f += vq * (tail if j % nt == nt - 1 else T)
+        return f * 4 * D
+
+    t0 = time.perf_counter()
+    oracle.sparse_causal_attention(ring, q, bits, T, scale, qtiles=[0])
+    one = time.perf_counter() - t0
+    n = max(1, min(nt - 1, int(target_s / max(one, 1e-3))))
+    tiles = list(range(1, 1 + n))
+    t0 = time.perf_counter()
+    oracle.sparse_causal_attention(ring, q, bits, T, scale, qtiles=tiles)
+    sec = time.perf_counter() - t0
+    return {
+        "value": kept_flops(tiles) / sec / 1e12,
+        "unit": "TFLOP/s",
+        "cores": len(os.sched_getaffinity(0)),
+        "kind": "oracle",
+        "sample": f"{wl.name}: head 0, query tiles 1..{n} of {nt} ({n * T} queries x {L * info.n_live} keys, "
+                  f"float64 numpy masked-dense), {sec:.1f} s; throughput in kept-tile FLOP/s",
+        "seconds": sec,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="1k", choices=["tiny", "480p", "1k", "2k"])
+    ap.add_argument("--secondary", default="2k", help="second workload reported in the same line ('' for none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the attention path has no multi-GPU variant here "
+              "(heads would shard across GPUs with no exchange inside the kernel)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_09150_amd as P
+    import synth
+
+    P.load()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    wl = synth.WORKLOADS[args.config]
+    res, state = run_workload(P, wl, args.steps, args.warmup)
+    line = {
+        "metric": METRIC,
+        "value": res["value"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}-shaped block-sparse chunk-causal attention",
+                   "batch": wl.batch, "heads": wl.heads, "head_dim": D, "chunk_tokens": wl.chunk_tokens,
+                   "grid": f"{wl.frames}x{wl.grid_h}x{wl.grid_w}", "tile": wl.tile,
+                   "window_chunks": wl.window_chunks, "keys": res["keys"], "p_prior": wl.p_prior,
+                   "pinned_first_chunk": wl.pin_sink},
+    }
+    for k in ("attn_ms", "attn_ms_p10", "attn_ms_p90", "attn_tflops", "append_us", "append_gbps", "lists_us",
+              "kept_tflop_per_step", "kept_fraction", "padded_tile_tflop_per_step"):
+        line[k] = res[k]
+    line["roofline"] = {
+        "bound": "mfma",
+        "achieved": res["attn_tflops"],
+        "peak": MFMA_BF16_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": res["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS,
+        "traffic": None,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, state, args.cpu_seconds)
+    del state
+    torch.cuda.empty_cache()
+    if args.secondary and args.secondary != args.config:
+        wl2 = synth.WORKLOADS[args.secondary]
+        res2, state2 = run_workload(P, wl2, max(5, args.steps // 2), args.warmup)
+        res2["roofline_frac"] = res2["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
+        line["secondary"] = res2
+        del state2
+        torch.cuda.empty_cache()
+    line["context"] = ("paper (whole cascade, not this kernel): ~30 FPS at 1K and ~18 FPS at 2K on a single "
+                       "B200, ~17 / ~10 FPS on a single H200")
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,195 @@
+/*
+ * uf.h -- C ABI of the MI355X (gfx950) block-sparse chunk-causal attention path.
+ *
+ * The operation (Ultra Flash, arXiv 2606.09150, Sec. 2.3.1 "Dynamic Block-Sparse
+ * Causal Attention", Eq. 4, and Sec. 2.3.2 "Dynamic Cache Management" (iii)):
+ * a video is generated chunk by chunk; every attention layer keeps a KV cache
+ * of earlier chunks (a compact window, App. C "KV cache: 3 temporal windows").
+ * The current chunk's queries attend, with scaled softmax attention, over the
+ * window's earlier chunks plus the current chunk (the temporal causal mask is
+ * chunk-granular: no token-level triangle inside a chunk), restricted per
+ * (head, query tile) to a kept subset of key tiles (the block mask of Eq. 4,
+ * executed by a block-sparse kernel that skips every other tile).
+ *
+ * Entry points, in the order one chunk uses them:
+ *   uf_kv_evict                 drop the oldest non-pinned chunks (host metadata)
+ *   uf_kv_append                copy the current chunk's K and V into a free slot
+ *   uf_build_tile_lists         per (b, h, query tile) keep lists of key tiles
+ *   uf_sparse_causal_attn_fwd   attention of the current chunk's queries
+ *
+ * Conventions
+ *   - bf16 tensors are raw IEEE bfloat16 bit patterns (uint16).
+ *   - Q, K, V, O are [B, L, H, D] contiguous, D fastest, L = chunk_tokens.
+ *   - Pointers named d_* are device pointers; the caller allocates and owns
+ *     every device buffer (pool, Q, K, V, O, LSE, lists).  The library owns only
+ *     the host-side handle; it never allocates device memory and never
+ *     synchronises a stream.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     device work is enqueued asynchronously on it; ring metadata changes at
+ *     enqueue time.  Work on other streams must be ordered by the caller.
+ *   - Every call returns a status code: UF_OK (0) or a negative UF_ERR_*.
+ *     Nothing aborts, throws or prints.  On error the handle is unchanged and
+ *     uf_last_error() describes the failure (thread-local text).
+ *   - A handle is not thread-safe; distinct handles are independent.
+ */
+#ifndef UF_H
+#define UF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define UF_OK               0
+#define UF_ERR_ARG         (-1)  /* null/misaligned pointer, bad size or value   */
+#define UF_ERR_UNSUPPORTED (-2)  /* valid but not built: head_dim != 128, tile not 64/128 */
+#define UF_ERR_CAPACITY    (-3)  /* append into a full window; pool too small     */
+#define UF_ERR_EMPTY       (-4)  /* evict more than evictable; work on no chunk   */
+#define UF_ERR_HIP         (-5)  /* a HIP launch failed; uf_last_error() has text */
+
+/* ---- flags (uf_kv_desc.flags) ----------------------------------------- */
+#define UF_F_DRYRUN     1u  /* metadata only: no device work is enqueued, device
+                               pointers are not dereferenced (host testing)  */
+#define UF_F_POISON_PAD 2u  /* fill padding rows of partial tiles with bf16 9984.0
+                               instead of 0 (checks that padding never counts) */
+
+#define UF_MAX_CHUNKS 64    /* largest window capacity */
+
+typedef struct uf_kv uf_kv; /* opaque host-side handle of one KV window */
+
+/* Window description.  The window holds at most max_chunks chunks of
+ * chunk_tokens tokens each, for batch x heads heads of dimension head_dim. */
+typedef struct {
+  int32_t batch;        /* B >= 1 */
+  int32_t heads;        /* H >= 1 */
+  int32_t head_dim;     /* D; must be 128 */
+  int32_t chunk_tokens; /* L >= 1: frames * grid_h * grid_w tokens per chunk */
+  int32_t tile;         /* T in {64, 128}: query tile = key tile = page rows */
+  int32_t max_chunks;   /* 1 .. UF_MAX_CHUNKS, pinned chunk and current one included */
+  int32_t pin_sink;     /* 1: the first appended chunk is never evicted */
+  uint32_t flags;       /* UF_F_* */
+} uf_kv_desc;
+
+/* Keep rule for uf_build_tile_lists.  For query tile i of head (b, h) and key
+ * tile t of the window chunk c:
+ *   kept  if c is the pinned chunk and keep_sink,
+ *   kept  if c is the current (most recently appended) chunk and keep_current,
+ *   else  kept iff (x >> 32) < thr, where x = seed and, for each field f of
+ *         (b, h, seq(current), i, seq(c), t) in turn, x = splitmix64(x ^ f);
+ *         thr = 2^32 when p_prior >= 1, else floor(p_prior * 2^32) in double.
+ * splitmix64(z): z += 0x9E3779B97F4A7C15, then z ^= z>>30, z *= 0xBF58476D1CE4E5B9,
+ * z ^= z>>27, z *= 0x94D049BB133111EB, z ^= z>>31 (mod 2^64; Steele, Lea and
+ * Flood, OOPSLA 2014).  This seeded Bernoulli rule stands in for the paper's
+ * content-adaptive top-k of Eq. 4 (not part of the paper).  seq() are append
+ * sequence numbers, so the lists depend only on the window's logical content. */
+typedef struct {
+  uint64_t seed;
+  double p_prior;       /* in [0, 1]; 1 keeps every tile (dense) */
+  int32_t keep_sink;    /* 0 or 1 */
+  int32_t keep_current; /* 0 or 1 */
+} uf_keep_rule;
+
+typedef struct {
+  int32_t n_live;     /* chunks in the window */
+  int32_t nq_tiles;   /* NT = ceil(L / T): query tiles = key tiles per chunk */
+  int32_t nk_tiles;   /* n_live * NT logical key tiles */
+  int32_t tail_valid; /* valid tokens of each chunk's last tile, L - (NT-1)*T */
+  int64_t first_seq;  /* seq of logical position 0, -1 if empty */
+  int64_t last_seq;   /* seq of the current chunk, -1 if empty */
+  int32_t has_sink;   /* 1 if logical position 0 is the pinned chunk */
+  int32_t nk_cap;     /* max_chunks * NT: row capacity of the lists */
+} uf_kv_info;
+
+/* Device list buffer layout (all offsets in bytes from d_lists; R = B*H*NT rows,
+ * row (b, h, i) = (b*H + h)*NT + i):
+ *   counts  int32 [R]               kept key tiles of the row
+ *   idx     int32 [R][nk_cap]       kept logical key tiles, ascending, then -1
+ *   mask    uint32[R][mask_words]   bit j%32 of word j/32 set iff tile j kept
+ * Logical key tile j is tile j % NT of the chunk at logical position j / NT;
+ * logical order is [pinned chunk][oldest earlier .. newest earlier][current]. */
+typedef struct {
+  size_t counts_offset;
+  size_t idx_offset;
+  size_t mask_offset;
+  size_t total_bytes;
+  int32_t rows;
+  int32_t nk_cap;
+  int32_t mask_words;
+  int32_t reserved;
+} uf_lists_layout;
+
+/* Pool bytes the window needs: max_chunks * B * H * NT pages of 4*T*D bytes.
+ * Page of (slot s, b, h, tile t) starts at ((((s*B + b)*H + h)*NT + t) * 4*T*D);
+ * it holds K as T rows of D bf16 (row r = token t*T + r of the chunk), then V
+ * transposed as D rows of T bf16 in which the keys of each group of 16 are
+ * stored with bits 2 and 3 of the key index swapped (column p holds key
+ * (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1)).  Rows past the chunk end are 0
+ * (9984.0 under UF_F_POISON_PAD).  Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED. */
+int uf_kv_pool_bytes(const uf_kv_desc* desc, size_t* bytes);
+
+/* Create a handle over a caller-owned pool (256-byte aligned, >= pool bytes).
+ * The pool must outlive the handle; its contents are written by append only.
+ * Errors: UF_ERR_ARG (null, misaligned, bad field), UF_ERR_UNSUPPORTED,
+ * UF_ERR_CAPACITY (pool_bytes too small). */
+int uf_kv_create(const uf_kv_desc* desc, void* d_pool, size_t pool_bytes, uf_kv** out);
+
+/* Destroy a handle (host memory only).  NULL is accepted. */
+int uf_kv_destroy(uf_kv* kv);
+
+/* Append the current chunk (Alg. 3, inference: the SR DiT attends over its KV
+ * cache plus the new chunk): copy K and V [B, L, H, D] bf16 (16-byte aligned)
+ * into the pages of a free slot; it becomes the current chunk with the next
+ * sequence number.  Errors: UF_ERR_ARG, UF_ERR_CAPACITY (window full), UF_ERR_HIP. */
+int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream);
+
+/* Drop the n oldest chunks that are not pinned (Sec. 2.3.2 (iii): a compact
+ * cache window).  Host metadata only: the freed slot is rewritten by a later
+ * append, which the stream orders after already-enqueued reads on that same
+ * stream.  n = 0 is a no-op.  Errors: UF_ERR_ARG (n < 0), UF_ERR_EMPTY (fewer
+ * than n evictable chunks). */
+int uf_kv_evict(uf_kv* kv, int32_t n_chunks);
+
+/* Window state.  Errors: UF_ERR_ARG. */
+int uf_kv_get_info(const uf_kv* kv, uf_kv_info* info);
+
+/* Slot and sequence number of logical position pos (0 <= pos < n_live).
+ * Errors: UF_ERR_ARG. */
+int uf_kv_logical(const uf_kv* kv, int32_t pos, int32_t* slot, int64_t* seq);
+
+/* Layout and size of the list buffer.  Errors: UF_ERR_ARG. */
+int uf_tile_lists_layout(const uf_kv* kv, uf_lists_layout* layout);
+int uf_tile_lists_bytes(const uf_kv* kv, size_t* bytes);
+
+/* Build the keep lists of the current window under `rule` into d_lists
+ * (256-byte aligned, >= uf_tile_lists_bytes).  Valid until the next append or
+ * evict.  Errors: UF_ERR_ARG, UF_ERR_EMPTY (no chunk), UF_ERR_HIP. */
+int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists,
+                        size_t bytes, void* stream);
+
+/* Block-sparse chunk-causal attention forward (Eq. 4 mask semantics): for each
+ * (b, h) and query row r of the current chunk in query tile i,
+ *   O[b,r,h,:] = sum_c softmax_c(scale * q.k_c) v_c over the tokens c of the
+ *   kept key tiles of row (b, h, i) (padding excluded), and
+ *   LSE[b,h,r] = natural log of sum_c exp(scale * q.k_c).
+ * A row with no kept tile gives O = 0 and LSE = -inf.  q, o: [B, L, H, D] bf16,
+ * 16-byte aligned; lse: [B, H, L] fp32 or NULL; d_lists as built by
+ * uf_build_tile_lists for the current window (entries naming a tile outside
+ * the window are skipped).  Computes in fp32 with bf16 MFMA products; O is
+ * rounded to nearest even.  Errors: UF_ERR_ARG, UF_ERR_EMPTY, UF_ERR_HIP. */
+int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists,
+                              float scale, void* d_o, float* d_lse, void* stream);
+
+/* Static text of a status code. */
+const char* uf_status_string(int status);
+
+/* Thread-local description of the last error returned on this thread. */
+const char* uf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UF_H */

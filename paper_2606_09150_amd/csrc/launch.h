@@ -1,0 +1,60 @@
+// Internal launch interface between the C ABI (uf_api.cpp) and the gfx950
+// kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/uf.h"
+
+namespace uf {
+
+// Bytes of one page: K [T][D] bf16 followed by V^T [D][T] bf16.
+__host__ __device__ inline size_t page_bytes(int T, int D) { return size_t(4) * size_t(T) * size_t(D); }
+
+// Column of key r inside its group of 16 in a V^T page row: bits 2 and 3
+// swapped.  The map is its own inverse.
+__host__ __device__ inline int swap23(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+struct AppendArgs {
+  const uint16_t* k;      // [B, L, H, D]
+  const uint16_t* v;      // [B, L, H, D]
+  uint8_t* pool;
+  int64_t slot;
+  int32_t B, H, L, T, NT, tail;
+  uint16_t pad;           // bf16 bits written into padding rows
+};
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
+
+struct ListArgs {
+  uint8_t* lists;
+  size_t idx_offset, mask_offset;
+  int32_t rows;           // B*H*NT
+  int32_t H, NT, nk, nk_cap, mask_words;
+  uint64_t seed;
+  uint64_t thr;           // 0 .. 2^32
+  int32_t keep_sink, keep_current;
+  int64_t cur_seq;
+  int64_t seq[UF_MAX_CHUNKS];   // per logical position
+  int32_t sink[UF_MAX_CHUNKS];  // 1 if logical position holds the pinned chunk
+};
+hipError_t launch_tile_lists(const ListArgs& a, hipStream_t stream);
+
+struct AttnArgs {
+  const uint16_t* q;      // [B, L, H, D]
+  uint16_t* o;            // [B, L, H, D]
+  float* lse;             // [B, H, L] or null
+  const uint8_t* pool;
+  const int32_t* counts;  // [rows]
+  const int32_t* idx;     // [rows][nk_cap]
+  int32_t B, H, L, T, NT, tail, nk, nk_cap;
+  float scale;            // softmax scale
+  float scale_log2;       // scale * log2(e)
+  int32_t slot_of[UF_MAX_CHUNKS];  // slot of each logical position
+};
+hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace uf

@@ -1,0 +1,305 @@
+// C ABI of the block-sparse chunk-causal attention path: argument validation,
+// the window (ring) metadata, and kernel launches.  See include/uf.h for the
+// contract of every entry point.
+//
+// The window realises the paper's compact SR KV cache window (Sec. 2.3.2,
+// dynamic cache management (iii); App. C "KV cache: 3 temporal windows") as a
+// fixed set of slots in a caller-owned pool: each live chunk occupies one slot;
+// logical order is ascending append sequence number, so an optional pinned
+// first chunk always sits at logical position 0; eviction frees the oldest
+// non-pinned slots and moves no data.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "launch.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_last_error[0] = '\0';
+  return UF_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct Live {
+  int32_t slot;
+  int64_t seq;
+  bool sink;
+};
+
+int check_desc(const uf_kv_desc* d) {
+  if (d == nullptr) return fail(UF_ERR_ARG, "desc is null");
+  if (d->batch < 1) return fail(UF_ERR_ARG, "batch must be >= 1 (got %d)", d->batch);
+  if (d->heads < 1) return fail(UF_ERR_ARG, "heads must be >= 1 (got %d)", d->heads);
+  if (d->chunk_tokens < 1) return fail(UF_ERR_ARG, "chunk_tokens must be >= 1 (got %d)", d->chunk_tokens);
+  if (d->max_chunks < 1 || d->max_chunks > UF_MAX_CHUNKS)
+    return fail(UF_ERR_ARG, "max_chunks must be in [1, %d] (got %d)", UF_MAX_CHUNKS, d->max_chunks);
+  if (d->pin_sink != 0 && d->pin_sink != 1) return fail(UF_ERR_ARG, "pin_sink must be 0 or 1");
+  if (d->flags & ~(UF_F_DRYRUN | UF_F_POISON_PAD)) return fail(UF_ERR_ARG, "unknown flag bits 0x%x", d->flags);
+  if (d->head_dim != 128) return fail(UF_ERR_UNSUPPORTED, "head_dim must be 128 (got %d)", d->head_dim);
+  if (d->tile != 64 && d->tile != 128) return fail(UF_ERR_UNSUPPORTED, "tile must be 64 or 128 (got %d)", d->tile);
+  // Index arithmetic in the kernels: element offsets are 64-bit, but list
+  // rows, page counts and token indices must fit in 31 bits.
+  const int64_t nt = (int64_t(d->chunk_tokens) + d->tile - 1) / d->tile;
+  const int64_t rows = int64_t(d->batch) * d->heads * nt;
+  const int64_t tokens = int64_t(d->batch) * d->chunk_tokens;
+  if (rows * d->max_chunks > INT32_MAX || tokens * d->heads > INT32_MAX)
+    return fail(UF_ERR_ARG, "shape too large: B*H*NT*max_chunks and B*L*H must fit in int32");
+  return UF_OK;
+}
+
+}  // namespace
+
+struct uf_kv {
+  uf_kv_desc d;
+  uint8_t* pool;
+  size_t pool_bytes;
+  int32_t nt;
+  int32_t tail;
+  int32_t nk_cap;
+  int32_t mask_words;
+  std::vector<Live> live;       // logical order
+  std::vector<uint8_t> used;    // per slot
+  int64_t next_seq;
+
+  bool dry() const { return (d.flags & UF_F_DRYRUN) != 0; }
+  int32_t rows() const { return d.batch * d.heads * nt; }
+  uf_lists_layout layout() const {
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    uf_lists_layout lay{};
+    lay.rows = rows();
+    lay.nk_cap = nk_cap;
+    lay.mask_words = mask_words;
+    lay.counts_offset = 0;
+    lay.idx_offset = up(size_t(lay.rows) * 4);
+    lay.mask_offset = lay.idx_offset + up(size_t(lay.rows) * size_t(nk_cap) * 4);
+    lay.total_bytes = lay.mask_offset + up(size_t(lay.rows) * size_t(mask_words) * 4);
+    return lay;
+  }
+};
+
+extern "C" {
+
+int uf_kv_pool_bytes(const uf_kv_desc* desc, size_t* bytes) {
+  if (int s = check_desc(desc)) return s;
+  if (bytes == nullptr) return fail(UF_ERR_ARG, "bytes is null");
+  const size_t nt = (size_t(desc->chunk_tokens) + desc->tile - 1) / desc->tile;
+  *bytes = size_t(desc->max_chunks) * desc->batch * desc->heads * nt * uf::page_bytes(desc->tile, desc->head_dim);
+  return ok();
+}
+
+int uf_kv_create(const uf_kv_desc* desc, void* d_pool, size_t pool_bytes, uf_kv** out) {
+  if (out == nullptr) return fail(UF_ERR_ARG, "out is null");
+  size_t need = 0;
+  if (int s = uf_kv_pool_bytes(desc, &need)) return s;
+  const bool dry = (desc->flags & UF_F_DRYRUN) != 0;
+  if (!dry && d_pool == nullptr) return fail(UF_ERR_ARG, "pool is null");
+  if (d_pool != nullptr && !aligned(d_pool, 256)) return fail(UF_ERR_ARG, "pool must be 256-byte aligned");
+  if (!dry && pool_bytes < need)
+    return fail(UF_ERR_CAPACITY, "pool has %zu bytes, window needs %zu", pool_bytes, need);
+  uf_kv* kv = new (std::nothrow) uf_kv();
+  if (kv == nullptr) return fail(UF_ERR_ARG, "out of host memory");
+  kv->d = *desc;
+  kv->pool = static_cast<uint8_t*>(d_pool);
+  kv->pool_bytes = pool_bytes;
+  kv->nt = (desc->chunk_tokens + desc->tile - 1) / desc->tile;
+  kv->tail = desc->chunk_tokens - (kv->nt - 1) * desc->tile;
+  kv->nk_cap = desc->max_chunks * kv->nt;
+  kv->mask_words = (kv->nk_cap + 31) / 32;
+  kv->used.assign(size_t(desc->max_chunks), 0);
+  kv->next_seq = 0;
+  *out = kv;
+  return ok();
+}
+
+int uf_kv_destroy(uf_kv* kv) {
+  delete kv;
+  return ok();
+}
+
+int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (int32_t(kv->live.size()) >= kv->d.max_chunks)
+    return fail(UF_ERR_CAPACITY, "window full (%d chunks)", kv->d.max_chunks);
+  int32_t slot = 0;
+  while (kv->used[size_t(slot)]) ++slot;
+  if (!kv->dry()) {
+    if (d_k == nullptr || d_v == nullptr) return fail(UF_ERR_ARG, "k or v is null");
+    if (!aligned(d_k, 16) || !aligned(d_v, 16)) return fail(UF_ERR_ARG, "k and v must be 16-byte aligned");
+    uf::AppendArgs a{};
+    a.k = static_cast<const uint16_t*>(d_k);
+    a.v = static_cast<const uint16_t*>(d_v);
+    a.pool = kv->pool;
+    a.slot = slot;
+    a.B = kv->d.batch;
+    a.H = kv->d.heads;
+    a.L = kv->d.chunk_tokens;
+    a.T = kv->d.tile;
+    a.NT = kv->nt;
+    a.tail = kv->tail;
+    a.pad = (kv->d.flags & UF_F_POISON_PAD) ? uint16_t(0x461C) : uint16_t(0);  // bf16 9984.0
+    hipError_t e = uf::launch_kv_append(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(UF_ERR_HIP, "kv_append launch: %s", hipGetErrorString(e));
+  }
+  const int64_t seq = kv->next_seq++;
+  kv->used[size_t(slot)] = 1;
+  kv->live.push_back(Live{slot, seq, kv->d.pin_sink == 1 && seq == 0});
+  return ok();
+}
+
+int uf_kv_evict(uf_kv* kv, int32_t n_chunks) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (n_chunks < 0) return fail(UF_ERR_ARG, "n_chunks must be >= 0 (got %d)", n_chunks);
+  int32_t evictable = 0;
+  for (const Live& c : kv->live) evictable += c.sink ? 0 : 1;
+  if (n_chunks > evictable)
+    return fail(UF_ERR_EMPTY, "asked to evict %d chunks, %d evictable", n_chunks, evictable);
+  std::vector<Live> keep;
+  keep.reserve(kv->live.size());
+  int32_t dropped = 0;
+  for (const Live& c : kv->live) {
+    if (!c.sink && dropped < n_chunks) {
+      kv->used[size_t(c.slot)] = 0;
+      ++dropped;
+    } else {
+      keep.push_back(c);
+    }
+  }
+  kv->live.swap(keep);
+  return ok();
+}
+
+int uf_kv_get_info(const uf_kv* kv, uf_kv_info* info) {
+  if (kv == nullptr || info == nullptr) return fail(UF_ERR_ARG, "null argument");
+  info->n_live = int32_t(kv->live.size());
+  info->nq_tiles = kv->nt;
+  info->nk_tiles = info->n_live * kv->nt;
+  info->tail_valid = kv->tail;
+  info->first_seq = kv->live.empty() ? -1 : kv->live.front().seq;
+  info->last_seq = kv->live.empty() ? -1 : kv->live.back().seq;
+  info->has_sink = (!kv->live.empty() && kv->live.front().sink) ? 1 : 0;
+  info->nk_cap = kv->nk_cap;
+  return ok();
+}
+
+int uf_kv_logical(const uf_kv* kv, int32_t pos, int32_t* slot, int64_t* seq) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (pos < 0 || pos >= int32_t(kv->live.size()))
+    return fail(UF_ERR_ARG, "logical position %d outside [0, %zu)", pos, kv->live.size());
+  if (slot) *slot = kv->live[size_t(pos)].slot;
+  if (seq) *seq = kv->live[size_t(pos)].seq;
+  return ok();
+}
+
+int uf_tile_lists_layout(const uf_kv* kv, uf_lists_layout* layout) {
+  if (kv == nullptr || layout == nullptr) return fail(UF_ERR_ARG, "null argument");
+  *layout = kv->layout();
+  return ok();
+}
+
+int uf_tile_lists_bytes(const uf_kv* kv, size_t* bytes) {
+  if (kv == nullptr || bytes == nullptr) return fail(UF_ERR_ARG, "null argument");
+  *bytes = kv->layout().total_bytes;
+  return ok();
+}
+
+int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists, size_t bytes,
+                        void* stream) {
+  if (kv == nullptr || rule == nullptr) return fail(UF_ERR_ARG, "null argument");
+  if (!(rule->p_prior >= 0.0 && rule->p_prior <= 1.0))
+    return fail(UF_ERR_ARG, "p_prior must lie in [0, 1]");
+  if ((rule->keep_sink != 0 && rule->keep_sink != 1) || (rule->keep_current != 0 && rule->keep_current != 1))
+    return fail(UF_ERR_ARG, "keep_sink and keep_current must be 0 or 1");
+  if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
+  const uf_lists_layout lay = kv->layout();
+  if (kv->dry()) return ok();
+  if (d_lists == nullptr || !aligned(d_lists, 256)) return fail(UF_ERR_ARG, "lists must be non-null and 256-byte aligned");
+  if (bytes < lay.total_bytes) return fail(UF_ERR_ARG, "lists buffer has %zu bytes, needs %zu", bytes, lay.total_bytes);
+  uf::ListArgs a{};
+  a.lists = static_cast<uint8_t*>(d_lists);
+  a.idx_offset = lay.idx_offset;
+  a.mask_offset = lay.mask_offset;
+  a.rows = lay.rows;
+  a.H = kv->d.heads;
+  a.NT = kv->nt;
+  a.nk = int32_t(kv->live.size()) * kv->nt;
+  a.nk_cap = kv->nk_cap;
+  a.mask_words = kv->mask_words;
+  a.seed = rule->seed;
+  a.thr = (rule->p_prior >= 1.0) ? (uint64_t(1) << 32) : uint64_t(std::floor(rule->p_prior * 4294967296.0));
+  a.keep_sink = rule->keep_sink;
+  a.keep_current = rule->keep_current;
+  a.cur_seq = kv->live.back().seq;
+  for (size_t p = 0; p < kv->live.size(); ++p) {
+    a.seq[p] = kv->live[p].seq;
+    a.sink[p] = kv->live[p].sink ? 1 : 0;
+  }
+  hipError_t e = uf::launch_tile_lists(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "tile_lists launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
+                              void* d_o, float* d_lse, void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (!std::isfinite(scale)) return fail(UF_ERR_ARG, "scale must be finite");
+  if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
+  if (kv->dry()) return ok();
+  if (d_q == nullptr || d_o == nullptr || d_lists == nullptr) return fail(UF_ERR_ARG, "q, o or lists is null");
+  if (!aligned(d_q, 16) || !aligned(d_o, 16)) return fail(UF_ERR_ARG, "q and o must be 16-byte aligned");
+  if (!aligned(d_lists, 256)) return fail(UF_ERR_ARG, "lists must be 256-byte aligned");
+  if (d_lse != nullptr && !aligned(d_lse, 4)) return fail(UF_ERR_ARG, "lse must be 4-byte aligned");
+  const uf_lists_layout lay = kv->layout();
+  uf::AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(d_q);
+  a.o = static_cast<uint16_t*>(d_o);
+  a.lse = d_lse;
+  a.pool = kv->pool;
+  a.counts = reinterpret_cast<const int32_t*>(static_cast<const uint8_t*>(d_lists) + lay.counts_offset);
+  a.idx = reinterpret_cast<const int32_t*>(static_cast<const uint8_t*>(d_lists) + lay.idx_offset);
+  a.B = kv->d.batch;
+  a.H = kv->d.heads;
+  a.L = kv->d.chunk_tokens;
+  a.T = kv->d.tile;
+  a.NT = kv->nt;
+  a.tail = kv->tail;
+  a.nk = int32_t(kv->live.size()) * kv->nt;
+  a.nk_cap = kv->nk_cap;
+  a.scale = scale;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  for (size_t p = 0; p < kv->live.size(); ++p) a.slot_of[p] = kv->live[p].slot;
+  hipError_t e = uf::launch_attn_fwd(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+const char* uf_status_string(int status) {
+  switch (status) {
+    case UF_OK: return "UF_OK";
+    case UF_ERR_ARG: return "UF_ERR_ARG: invalid argument";
+    case UF_ERR_UNSUPPORTED: return "UF_ERR_UNSUPPORTED: configuration not built";
+    case UF_ERR_CAPACITY: return "UF_ERR_CAPACITY: window or pool full";
+    case UF_ERR_EMPTY: return "UF_ERR_EMPTY: not enough chunks";
+    case UF_ERR_HIP: return "UF_ERR_HIP: HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* uf_last_error(void) { return g_last_error; }
+
+}  // extern "C"

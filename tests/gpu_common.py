@@ -1,0 +1,105 @@
+"""Shared helpers of the GPU parity tests: build the same window on the GPU
+(through the C ABI) and in the oracle, and compare results.
+
+Error metric for bf16 outputs (the spec bar of 1e-2): per (b, h, query
+row), max_d |O_gpu - O_ref| / max_d |O_ref|.  With N(0,1) inputs the outputs
+are small (about 1/sqrt(number of kept keys)), so a raw elementwise ratio
+would be ill-posed; the row-normalised form is the one bounded here.
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+REL_TOL = 1e-2     # max relative error per row on bf16 O
+LSE_TOL = 2e-3     # absolute error on the fp32 log-sum-exp
+
+
+def require_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_09150_amd as P
+    P.load()   # raises if libuf.so is missing: no fallback
+    return P
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def row_rel_err(o_gpu, o_ref):
+    """max over rows of max_d|diff| / max_d|ref|; arrays [..., D]."""
+    diff = np.abs(o_gpu - o_ref).max(axis=-1)
+    ref = np.abs(o_ref).max(axis=-1)
+    return float((diff / np.maximum(ref, 1e-30)).max())
+
+
+class Case:
+    """One window driven identically on the GPU and in the oracle."""
+
+    def __init__(self, P, B, L, H, T, max_chunks, pin_sink, seed, flags=0, gen_device="cpu",
+                 oracle_heads=None):
+        self.P = P
+        self.B, self.L, self.H, self.T = B, L, H, T
+        self.seed = seed
+        self.win = P.KVWindow(B, H, L, T, max_chunks, pin_sink, flags=flags)
+        self.ring = oracle.RingModel(max_chunks, pin_sink)
+        self.gen_device = gen_device
+        self.oracle_heads = oracle_heads   # None: all heads in the oracle
+        self.n_appended = 0
+
+    def _draw(self, chunk, name):
+        t = synth.custom_tensor((self.B, self.L, self.H, 128), self.seed, chunk, name, device=self.gen_device)
+        return t.cuda() if not t.is_cuda else t
+
+    def _host(self, t):
+        if self.oracle_heads is not None:
+            t = t[:, :, self.oracle_heads, :]
+        return f64(t)
+
+    def append(self, evict_when_full=True):
+        if evict_when_full and self.win.info().n_live == self.win.desc.max_chunks:
+            self.win.evict(1)
+            self.ring.evict(1)
+        k = self._draw(self.n_appended, "k")
+        v = self._draw(self.n_appended, "v")
+        self.win.append(k, v)
+        self.ring.append(self._host(k), self._host(v))
+        self.n_appended += 1
+        return k, v
+
+    def query(self):
+        return self._draw(self.n_appended - 1, "q")
+
+    def rule(self, p, keep_sink=True, keep_current=True, seed=None):
+        return oracle.KeepRule(self.seed if seed is None else seed, p, keep_sink, keep_current)
+
+    def oracle_bits(self, rule):
+        """Keep bits [B, H_all, NT, NK] from window metadata (all heads)."""
+        meta = oracle.RingModel(self.ring.max_chunks, self.ring.pin_sink)
+        meta.live = [oracle.ring.Chunk(c.seq, c.sink, np.broadcast_to(np.zeros(1), (self.B, self.L, self.H, 1)),
+                                       None) for c in self.ring.live]
+        return oracle.keep_bits(meta, self.T, rule)
+
+    def gpu_lists(self, rule):
+        self.win.build_lists(rule.seed, rule.p_prior, rule.keep_sink, rule.keep_current)
+        torch.cuda.synchronize()
+        c, i, m = self.win.lists_views()
+        return c.cpu().numpy(), i.cpu().numpy(), m.cpu().numpy().view(np.uint32)
+
+    def attention(self, q, scale=None):
+        scale = 1.0 / math.sqrt(128) if scale is None else scale
+        o, lse = self.win.attention(q, scale)
+        torch.cuda.synchronize()
+        return o, lse

@@ -1,0 +1,61 @@
+"""uf_kv_append: pages read back bit for bit against the layout documented in
+include/uf.h (K rows, V transposed with swap23 key order, padded tails)."""
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from tests.gpu_common import log, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _swap23(p):
+    return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1)
+
+
+def _bits(t):
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("B,L,H,T,poison", [(1, 192, 2, 64, False), (2, 300, 3, 128, False),
+                                            (1, 300, 2, 128, True), (1, 130, 1, 64, True)])
+def test_pages_read_back(B, L, H, T, poison):
+    P = require_gpu()
+    log(f"append B={B} L={L} H={H} T={T} poison={poison}")
+    flags = P._lib.UF_F_POISON_PAD if poison else 0
+    win = P.KVWindow(B, H, L, T, 3, True, flags=flags)
+    chunks = {}
+    for c in range(5):
+        if win.info().n_live == 3:
+            win.evict(1)
+        k = synth.custom_tensor((B, L, H, 128), 99, c, "k").cuda()
+        v = synth.custom_tensor((B, L, H, 128), 99, c, "v").cuda()
+        win.append(k, v)
+        chunks[c] = (_bits(k), _bits(v))
+    torch.cuda.synchronize()
+    pool = win.pool.cpu().numpy()
+    info = win.info()
+    nt, tail = info.nq_tiles, info.tail_valid
+    pad = 0x461C if poison else 0
+    D = 128
+    page = 4 * T * D
+    assert info.n_live == 3
+    for pos in range(info.n_live):
+        slot, seq = win.logical(pos)
+        kb, vb = chunks[seq]
+        for b in range(B):
+            for h in range(H):
+                for t in range(nt):
+                    off = (((slot * B + b) * H + h) * nt + t) * page
+                    kpage = pool[off:off + 2 * T * D].view(np.uint16).reshape(T, D)
+                    vpage = pool[off + 2 * T * D:off + page].view(np.uint16).reshape(D, T)
+                    valid = tail if t == nt - 1 else T
+                    assert np.array_equal(kpage[:valid], kb[b, t * T:t * T + valid, h, :])
+                    assert (kpage[valid:] == pad).all()
+                    keys = np.array([_swap23(p) for p in range(T)])
+                    want_v = np.full((D, T), pad, dtype=np.uint16)
+                    ok = keys < valid
+                    want_v[:, ok] = vb[b, t * T + keys[ok], h, :].T
+                    assert np.array_equal(vpage, want_v)

@@ -1,0 +1,178 @@
+"""Host-side tests of the C ABI (no GPU): exported symbols, the window's
+metadata against the oracle's window model under random append/evict
+scripts (dry-run mode), and every error path that the host can force."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "uf.h")
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2606_09150_amd as pkg
+    from paper_2606_09150_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("libuf.so is not built (python -m paper_2606_09150_amd.build)")
+    pkg.load()
+    return pkg
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(uf_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol(P):
+    from paper_2606_09150_amd import _lib
+    names = _declared()
+    assert len(names) == 13
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True).stdout
+    exported = sorted(set(re.findall(r"\sT\s(uf_\w+)$", out, re.M)))
+    assert exported == names
+    assert set(_lib._SIGNATURES) == set(names)
+
+
+def _dry(P, max_chunks=5, pin_sink=True, L=300, T=128, B=1, H=2):
+    return P.KVWindow(B, H, L, T, max_chunks, pin_sink, flags=P._lib.UF_F_DRYRUN)
+
+
+@pytest.mark.parametrize("pin_sink", [True, False])
+@pytest.mark.parametrize("seed", range(6))
+def test_dry_run_window_matches_oracle_model(P, pin_sink, seed):
+    rng = np.random.default_rng(seed)
+    max_chunks = int(rng.integers(1, 7))
+    w = _dry(P, max_chunks=max_chunks, pin_sink=pin_sink)
+    model = oracle.RingModel(max_chunks, pin_sink)
+    z = np.zeros((1, 1, 1, 1))
+    for _ in range(60):
+        if rng.random() < 0.6:
+            try:
+                model.append(z, z)
+                want = None
+            except oracle.RingCapacityError:
+                want = P._lib.UF_ERR_CAPACITY
+            try:
+                w.append(None, None)
+                got = None
+            except P.UfError as e:
+                got = e.status
+        else:
+            n = int(rng.integers(0, 4))
+            try:
+                model.evict(n)
+                want = None
+            except oracle.RingEmptyError:
+                want = P._lib.UF_ERR_EMPTY
+            try:
+                w.evict(n)
+                got = None
+            except P.UfError as e:
+                got = e.status
+        assert got == want
+        info = w.info()
+        chunks = model.logical_chunks()
+        assert info.n_live == len(chunks)
+        assert info.nk_tiles == len(chunks) * info.nq_tiles
+        seqs = [w.logical(p)[1] for p in range(info.n_live)]
+        assert seqs == [c.seq for c in chunks]
+        slots = [w.logical(p)[0] for p in range(info.n_live)]
+        assert len(set(slots)) == len(slots) and all(0 <= s < max_chunks for s in slots)
+        assert info.has_sink == int(bool(chunks) and chunks[0].sink)
+        assert info.first_seq == (chunks[0].seq if chunks else -1)
+        assert info.last_seq == (chunks[-1].seq if chunks else -1)
+
+
+def test_geometry_and_layout(P):
+    w = _dry(P, max_chunks=5, L=24480, T=128, H=12)
+    info = w.info()
+    assert (info.nq_tiles, info.tail_valid, info.nk_cap) == (192, 32, 960)
+    lay = w.layout
+    rows = 12 * 192
+    assert lay.rows == rows and lay.nk_cap == 960 and lay.mask_words == 30
+    assert lay.counts_offset == 0 and lay.idx_offset % 256 == 0 and lay.mask_offset % 256 == 0
+    assert lay.idx_offset >= 4 * rows
+    assert lay.mask_offset >= lay.idx_offset + 4 * rows * 960
+    assert lay.total_bytes >= lay.mask_offset + 4 * rows * 30
+    assert w.pool_bytes == 5 * 12 * 192 * 4 * 128 * 128
+
+
+def test_error_paths(P):
+    L = P._lib
+    E = P.UfError
+
+    def status(fn, *a):
+        with pytest.raises(E) as ei:
+            fn(*a)
+        return ei.value.status
+
+    base = dict(batch=1, heads=2, chunk_tokens=100, tile=128, max_chunks=3, pin_sink=1, head_dim=128, flags=0)
+    bad = [
+        (dict(batch=0), L.UF_ERR_ARG), (dict(heads=0), L.UF_ERR_ARG), (dict(chunk_tokens=0), L.UF_ERR_ARG),
+        (dict(max_chunks=0), L.UF_ERR_ARG), (dict(max_chunks=65), L.UF_ERR_ARG), (dict(pin_sink=2), L.UF_ERR_ARG),
+        (dict(flags=8), L.UF_ERR_ARG), (dict(head_dim=64), L.UF_ERR_UNSUPPORTED),
+        (dict(tile=32), L.UF_ERR_UNSUPPORTED), (dict(batch=1 << 20, heads=1 << 10), L.UF_ERR_ARG),
+    ]
+    for change, code in bad:
+        d = L.make_desc(**{**base, **change})
+        assert status(L.uf_kv_pool_bytes, d) == code
+    d = L.make_desc(**base)
+    need = L.uf_kv_pool_bytes(d)
+
+    class FakePtr:  # an aligned address that is never dereferenced on these paths
+        def __init__(self, p):
+            self.p = p
+
+        def data_ptr(self):
+            return self.p
+
+    assert status(L.uf_kv_create, d, None, need) == L.UF_ERR_ARG
+    assert status(L.uf_kv_create, d, FakePtr(0x10000 + 8), need) == L.UF_ERR_ARG
+    assert status(L.uf_kv_create, d, FakePtr(0x10000), need - 1) == L.UF_ERR_CAPACITY
+    h = L.uf_kv_create(d, FakePtr(0x10000), need)
+    try:
+        # no chunk yet
+        assert status(L.uf_sparse_causal_attn_fwd, h, FakePtr(0x20000), FakePtr(0x30000), 0.1,
+                      FakePtr(0x40000), None, 0) == L.UF_ERR_EMPTY
+        rule = L.uf_keep_rule(1, 0.5, 1, 1)
+        assert status(L.uf_build_tile_lists, h, rule, FakePtr(0x30000), 1 << 20, 0) == L.UF_ERR_EMPTY
+        assert status(L.uf_kv_evict, h, 1) == L.UF_ERR_EMPTY
+        assert status(L.uf_kv_evict, h, -1) == L.UF_ERR_ARG
+        # append argument checks happen before any launch
+        assert status(L.uf_kv_append, h, None, FakePtr(0x20000), 0) == L.UF_ERR_ARG
+        assert status(L.uf_kv_append, h, FakePtr(0x20008), FakePtr(0x20000), 0) == L.UF_ERR_ARG
+        assert L.uf_kv_get_info(h).n_live == 0
+        assert status(L.uf_kv_logical, h, 0) == L.UF_ERR_ARG
+    finally:
+        L.uf_kv_destroy(h)
+    # rule and scale checks on a dry-run window that holds a chunk
+    w = _dry(P, max_chunks=2)
+    w.append(None, None)
+    for p in (-0.1, 1.5, float("nan")):
+        assert status(L.uf_build_tile_lists, w.handle, L.uf_keep_rule(1, p, 1, 1), None, 0) == L.UF_ERR_ARG
+    assert status(L.uf_build_tile_lists, w.handle, L.uf_keep_rule(1, 0.5, 2, 1), None, 0) == L.UF_ERR_ARG
+    L.uf_build_tile_lists(w.handle, L.uf_keep_rule(1, 0.5, 1, 1), None, 0)
+    assert status(L.uf_sparse_causal_attn_fwd, w.handle, None, None, float("inf"), None) == L.UF_ERR_ARG
+    L.uf_sparse_causal_attn_fwd(w.handle, None, None, 0.1, None)
+    w.append(None, None)
+    assert status(L.uf_kv_append, w.handle, None, None) == L.UF_ERR_CAPACITY
+    assert status(L.uf_kv_evict, w.handle, 2) == L.UF_ERR_EMPTY   # the pinned chunk is not evictable
+    w.evict(1)
+    assert w.info().n_live == 1 and w.info().has_sink == 1
+    # status strings and the null handle
+    assert L.uf_status_string(0) == "UF_OK"
+    for code in (L.UF_ERR_ARG, L.UF_ERR_UNSUPPORTED, L.UF_ERR_CAPACITY, L.UF_ERR_EMPTY, L.UF_ERR_HIP):
+        assert L.uf_status_string(code).startswith("UF_ERR_")
+    assert status(L.uf_kv_evict, None, 1) == L.UF_ERR_ARG
+    assert "null" in L.uf_last_error()
