@@ -4,26 +4,43 @@
 // list in ascending logical order (Eq. 4: attention restricted to the kept
 // blocks of the chunk-causal window) and keeps an online softmax.
 //
-// Work split: 32 queries per wave, T/32 waves per workgroup.  The kernel
-// computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (K from LDS as the A
-// operand, Q held in registers as the B operand), so in the result layout
-// every lane owns one query column and 16 key rows per 32-key block; the row
-// max and row sum need one exchange with the partner lane (permlane32 swap).
-// The exponentiated scores are rounded to bf16 in place and reused directly as
-// the B operand of O^T += V^T P^T; V pages are stored transposed with the keys
-// of each group of 16 in swap23 order, which is exactly the k-slot order in
-// which the S^T result lanes hold them.  Softmax runs in base 2 with
-// scale*log2(e) folded into one FMA.  fp32 accumulation throughout; O is
-// normalised once at the end and rounded to bf16 (nearest even).
+// Work split: 32 queries per wave, T/32 waves per workgroup, two workgroups
+// resident per CU (two waves per SIMD, so one wave's MFMA work overlaps the
+// other's softmax VALU work).  The kernel computes S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16 (K from LDS as the A operand, Q held in registers as
+// the B operand), so in the result layout every lane owns one query column and
+// 16 key rows per 32-key block; the row max and row sum need one exchange with
+// the partner lane (permlane32 swap).  The exponentiated scores are rounded to
+// bf16 in place and reused directly as the B operand of O^T += V^T P^T; V pages
+// are stored transposed with the keys of each group of 16 in swap23 order,
+// which is exactly the k-slot order in which the S^T result lanes hold them.
+//
+// Memory pipeline: pages are copied HBM -> LDS by direct global_load_lds
+// (16 bytes per lane, no register staging) into one K buffer and one V buffer
+// with an XOR swizzle of 16-byte chunks (conflict-free MFMA operand reads).
+// K of the next tile is requested as soon as every wave has read the current
+// K (so it lands during softmax and PV); V of the next tile as soon as every
+// wave has read the current V (so it lands during the next S).
+//
+// Softmax runs in base 2 with scale*log2(e) folded into one FMA.  The running
+// max is raised lazily: O and l are rescaled only when some lane's tile max
+// exceeds its running max by more than 8 (base-2 units), so exponentials stay
+// <= 2^8 and the rescale is rare.  Row sums add the bf16-rounded weights that
+// the PV product uses (v_dot2_f32_bf16).  O is normalised once at the end and
+// rounded to bf16 (nearest even).
 #include "../launch.h"
 
 namespace uf {
 namespace {
 
 constexpr int kD = 128;
+constexpr float kLazyLog2 = 8.0f;   // rescale when the max grows by more than 2^8
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(4))) int32_t const_i32;   // uniform -> scalar loads
 
 __device__ inline bf16x8 as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8, u); }
 
@@ -38,19 +55,36 @@ __device__ inline float pair_sum(float x) {
 }
 
 __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+  bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
+// One 16-byte-per-lane copy global -> LDS: lane l reads base + off and writes
+// LDS byte lds + 16*l.  Issued as inline assembly so that the compiler's
+// wait-count insertion does not treat every later LDS read as dependent on it;
+// the kernel orders the copies with explicit s_waitcnt vmcnt and barriers.
+// The uniform base is a scalar pair and the LDS target goes through m0.
+__device__ inline void dma16(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(off), "s"(base), "s"(lds) : "memory");
+}
+
+// s_waitcnt immediates (gfx9 encoding): vmcnt in [3:0] and [15:14], expcnt
+// in [6:4], lgkmcnt in [11:8].
+constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+constexpr int kWaitLgkm0 = 15 | (7 << 4) | (0 << 8) | (3 << 14);
+
 template <int T>
-__global__ __launch_bounds__(T * 2) void attn_fwd_kernel(AttnArgs a) {
+__global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
   constexpr int kWaves = T / 32;
   constexpr int kThreads = kWaves * 64;
-  constexpr int KB = T / 32;              // 32-key blocks per key tile
-  constexpr int kKChunks = kD / 8;        // 16-byte chunks per K row
-  constexpr int kVChunks = T / 8;         // 16-byte chunks per V^T row
-  __shared__ uint4 sK[T * kKChunks];
-  __shared__ uint4 sV[kD * kVChunks];
+  constexpr int KB = T / 32;                       // 32-key blocks per key tile
+  constexpr int kKC = kD / 8;                      // 16-byte chunks per K row
+  constexpr int kVC = T / 8;                       // 16-byte chunks per V^T row
+  constexpr int kKLoads = T * kKC / kThreads;      // direct loads per lane for a K tile
+  constexpr int kVLoads = kD * kVC / kThreads;     // and for a V tile
+  static_assert(kKLoads == 8 && kVLoads == 8, "load split");
+  __shared__ uint4 sK[T * kKC];
+  __shared__ uint4 sV[kD * kVC];
 
   const int row = blockIdx.x;
   const int qt = row % a.NT;
@@ -58,7 +92,7 @@ __global__ __launch_bounds__(T * 2) void attn_fwd_kernel(AttnArgs a) {
   const int h = bh % a.H;
   const int b = bh / a.H;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int g = lane >> 5;
   const int ln = lane & 31;
@@ -75,52 +109,103 @@ __global__ __launch_bounds__(T * 2) void attn_fwd_kernel(AttnArgs a) {
       if (qvalid) u = *reinterpret_cast<const uint4*>(qp + 16 * ks);
       qf[ks] = as_bf16x8(u);
     }
+    // Q is in registers before any page copy is issued, so that the only
+    // vector-memory operations in flight inside the loop are page copies.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   }
 
   f32x16 o[kD / 32];
 #pragma unroll
   for (int mb = 0; mb < kD / 32; ++mb) o[mb] = f32x16{};
-  float m = -INFINITY;   // running max of raw scores q.k
-  float l = 0.f;         // running sum of exp(scale * (s - m))
+  float m = -INFINITY;   // running (lazily raised) max of raw scores q.k
+  float l = 0.f;         // running sum of bf16(exp2((s - m) * c2))
 
-  const int count = a.counts[row];
-  const int32_t* list = a.idx + size_t(row) * a.nk_cap;
+  const int count = ((const const_i32*)a.counts)[row];
+  const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
   const size_t pbytes = page_bytes(T, kD);
+  const uint8_t* head_pages = a.pool + (size_t(b) * a.H + h) * a.NT * pbytes;
+  const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
   const float c2 = a.scale_log2;
+  const float lazy_raw = kLazyLog2 / fabsf(c2);
 
-  for (int n = 0; n < count; ++n) {
+  // Entries naming a tile outside the window (stale lists) are skipped.
+  auto next_valid = [&](int n) {
+    while (n < count && unsigned(list[n]) >= unsigned(a.nk)) ++n;
+    return n;
+  };
+  auto page_of = [&](int n) {
     const int j = list[n];
-    if (unsigned(j) >= unsigned(a.nk)) continue;   // stale entry: outside the window
     const int pos = j / a.NT;
     const int t = j - pos * a.NT;
-    const uint4* page = reinterpret_cast<const uint4*>(
-        a.pool + ((size_t(a.slot_of[pos]) * a.B + b) * a.H + h) * a.NT * pbytes + size_t(t) * pbytes);
-    const int valid = (t == a.NT - 1) ? a.tail : T;
+    return head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
+  };
+  // Direct HBM -> LDS copies.  Instruction i of wave w fills the 64 chunks
+  // [64*(i*kWaves + w), +64) of a buffer; lane l of it fetches the page chunk
+  // that the XOR swizzle assigns to that LDS position.  K rows and V^T rows
+  // share the geometry when T = 128; the per-lane byte offsets are loop
+  // invariant.
+  uint32_t koff[kKLoads], voff[kVLoads];
+#pragma unroll
+  for (int i = 0; i < kKLoads; ++i) {
+    const int p = (i * kWaves + wave) * 64 + lane;
+    const int r = p / kKC, c = p % kKC;
+    koff[i] = uint32_t(r * kKC + (c ^ (r & 15))) * 16u;
+  }
+#pragma unroll
+  for (int i = 0; i < kVLoads; ++i) {
+    const int p = (i * kWaves + wave) * 64 + lane;
+    const int d = p / kVC, c = p % kVC;
+    voff[i] = uint32_t(d * kVC + (c ^ (d & (kVC - 1)))) * 16u;
+  }
+  const uint32_t k_lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)sK) + wave * 1024u;
+  const uint32_t v_lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)sV) + wave * 1024u;
+  auto issue_k = [&](const uint8_t* page) {
+#pragma unroll
+    for (int i = 0; i < kKLoads; ++i) dma16(page, koff[i], k_lds + uint32_t(i * kWaves) * 1024u);
+  };
+  auto issue_v = [&](const uint8_t* page) {
+    const uint8_t* vpage = page + size_t(T) * kD * 2;
+#pragma unroll
+    for (int i = 0; i < kVLoads; ++i) dma16(vpage, voff[i], v_lds + uint32_t(i * kWaves) * 1024u);
+  };
 
-    __syncthreads();
-    for (int c = tid; c < T * kKChunks; c += kThreads) {
-      const int r = c / kKChunks, cc = c % kKChunks;
-      sK[r * kKChunks + (cc ^ (r & 15))] = page[c];
-    }
-    for (int c = tid; c < kD * kVChunks; c += kThreads) {
-      const int d = c / kVChunks, cc = c % kVChunks;
-      sV[d * kVChunks + (cc ^ (d & (kVChunks - 1)))] = page[T * kKChunks + c];
-    }
-    __syncthreads();
+  int n = next_valid(0);
+  if (n < count) {
+    const uint8_t* p0 = page_of(n);
+    issue_k(p0);
+    issue_v(p0);
+  }
+  while (n < count) {
+    const int nn = next_valid(n + 1);
+    const bool has_next = nn < count;
+    const int t_cur = list[n] % a.NT;
+    const int valid = (t_cur == a.NT - 1) ? a.tail : T;
+    const uint8_t* pnext = has_next ? page_of(nn) : nullptr;
+
+    // K_n has landed once only V_n's loads may still be outstanding.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(kVLoads));
+    __builtin_amdgcn_s_barrier();
 
     // S^T = K Q^T : KB blocks of 32 keys x 32 queries.
     f32x16 s[KB];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      s[kb] = f32x16{};
-      const int r = kb * 32 + ln;
+    for (int kb = 0; kb < KB; ++kb) s[kb] = f32x16{};
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int ks = 0; ks < kD / 16; ++ks) {
+    for (int ks = 0; ks < kD / 16; ++ks) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const int r = kb * 32 + ln;
         const int cc = 2 * ks + g;
-        const bf16x8 kf = as_bf16x8(sK[r * kKChunks + (cc ^ (r & 15))]);
+        const bf16x8 kf = as_bf16x8(sK[r * kKC + (cc ^ (r & 15))]);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[kb], 0, 0, 0);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
+    // every wave has its K operands in registers: the K buffer can be refilled
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+    if (has_next) issue_k(pnext);
 
     // Padding keys of a chunk's last tile never count.
     if (valid < T) {
@@ -139,51 +224,63 @@ __global__ __launch_bounds__(T * 2) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[kb][e]);
     mx = pair_max(mx);
-    const float mnew = fmaxf(m, mx);
-    const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((m - mnew) * c2);
-    const float mb2 = mnew * c2;
-    float rs = 0.f;
+    if (__ballot(mx > m + lazy_raw) != 0) {
+      const float mnew = fmaxf(m, mx);
+      const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((m - mnew) * c2);
+      m = mnew;
+      l *= alpha;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], c2, -mb2));
-        s[kb][e] = p;
-        rs += p;
-      }
-    rs = pair_sum(rs);
-    l = l * alpha + rs;
-    m = mnew;
-#pragma unroll
-    for (int mb = 0; mb < kD / 32; ++mb) o[mb] *= alpha;
+      for (int mb = 0; mb < kD / 32; ++mb) o[mb] *= alpha;
+    }
+    const float mb2 = m * c2;
 
     // P^T as the B operand: 16-key halves of each 32-key block.
     bf16x8 pf[KB][2];
+    float rs = 0.f;
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        uint4 u;
-        u.x = pack_bf16x2(s[kb][8 * hh + 0], s[kb][8 * hh + 1]);
-        u.y = pack_bf16x2(s[kb][8 * hh + 2], s[kb][8 * hh + 3]);
-        u.z = pack_bf16x2(s[kb][8 * hh + 4], s[kb][8 * hh + 5]);
-        u.w = pack_bf16x2(s[kb][8 * hh + 6], s[kb][8 * hh + 7]);
-        pf[kb][hh] = as_bf16x8(u);
+        bf16x2 pr[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][8 * hh + 2 * e], c2, -mb2));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][8 * hh + 2 * e + 1], c2, -mb2));
+          pr[e] = bf16x2{(__bf16)p0, (__bf16)p1};
+          rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], ones, rs, false);
+        }
+        pf[kb][hh] = __builtin_shufflevector(__builtin_shufflevector(pr[0], pr[1], 0, 1, 2, 3),
+                                             __builtin_shufflevector(pr[2], pr[3], 0, 1, 2, 3),
+                                             0, 1, 2, 3, 4, 5, 6, 7);
       }
+    l += pair_sum(rs);
+
+    // V_n has landed once only K_{n+1}'s loads may still be outstanding.
+    if (has_next)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(kKLoads));
+    else
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __builtin_amdgcn_s_barrier();
 
     // O^T += V^T P^T : 4 blocks of 32 dims x 32 queries.
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-    for (int mb = 0; mb < kD / 32; ++mb) {
-      const int d = mb * 32 + ln;
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
+        for (int mb = 0; mb < kD / 32; ++mb) {
+          const int d = mb * 32 + ln;
           const int cc = 2 * (2 * kb + hh) + g;
-          const bf16x8 vf = as_bf16x8(sV[d * kVChunks + (cc ^ (d & (kVChunks - 1)))]);
+          const bf16x8 vf = as_bf16x8(sV[d * kVC + (cc ^ (d & (kVC - 1)))]);
           o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hh], o[mb], 0, 0, 0);
         }
-    }
+    __builtin_amdgcn_s_setprio(0);
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+    if (has_next) issue_v(pnext);
+    n = nn;
   }
 
   if (qvalid) {
