@@ -189,6 +189,9 @@ def main():
     ap.add_argument("--secondary", default="2k", help="second workload reported in the same line ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the run, copy a buffer of this many MiB three times with a plain device copy "
+                         "(reference dispatches for scaling hardware byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -250,6 +253,15 @@ def main():
         line["secondary"] = res2
         del state2
         torch.cuda.empty_cache()
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        line["calib_copy_bytes"] = n
+        del src, dst
     line["context"] = ("paper (whole cascade, not this kernel): ~30 FPS at 1K and ~18 FPS at 2K on a single "
                        "B200, ~17 / ~10 FPS on a single H200")
     print(json.dumps(line), flush=True)

@@ -1,0 +1,361 @@
+// attn_fwd (128-token tiles): block-sparse chunk-causal attention forward on
+// gfx950 with a key-split ping-pong between two wave groups.
+//
+// For one (b, h, query tile i) the workgroup walks the kept key tiles of its
+// list in ascending logical order (Eq. 4: attention restricted to the kept
+// blocks of the chunk-causal window) and keeps an online softmax.
+//
+// Work split.  Eight waves per workgroup, one workgroup per CU, two waves per
+// SIMD.  Waves w and w+4 own the same 32 queries; group A (waves 0-3) takes
+// keys 0..63 of every kept tile, group B (waves 4-7) keys 64..127, each with
+// its own running max, sum and O.  The two partial states are merged through
+// LDS at the end (flash-decoding style log-sum-exp merge).
+//
+// Ping-pong.  Per tile there are two phases separated by workgroup barriers.
+// In one phase group A issues its MFMA work (PV of the previous tile, S of the
+// current one) while group B runs its softmax VALU work, in the next phase the
+// roles swap; the two waves sharing a SIMD therefore alternate between the
+// matrix core and the vector ALU instead of contending for one of them.
+//
+// Products.  S^T = K Q^T and O^T += V^T P^T on v_mfma_f32_32x32x16_bf16: K and
+// V^T come from LDS as the A operand, Q^T and P^T are B operands held in
+// registers; every lane owns one query column, so the row max and row sum
+// need one exchange with the partner lane (permlane32 swap), and the
+// exponentiated scores are rounded to bf16 in place to serve as the PV operand
+// (V pages store the keys of each group of 16 in swap23 order, which is the
+// k-slot order of the S^T result lanes).
+//
+// Memory.  Whole tiles are copied HBM -> LDS by direct global_load_lds
+// (16 bytes per lane, XOR-swizzled 16-byte chunks, conflict-free operand
+// reads) into two K and two V tile buffers (128 KB).  At the start of phase
+// 2m the K tile m+1 and the V tile m are requested; each is first read two
+// phases later.
+//
+// Softmax in base 2 with scale*log2(e) folded into one FMA; the running max is
+// raised lazily (only when it grows by more than 2^8); row sums add the
+// bf16-rounded weights (v_dot2_f32_bf16).
+#include "attn_common.h"
+
+#include <type_traits>
+
+namespace uf {
+namespace {
+
+using namespace attn;
+
+constexpr int kT = 128;
+constexpr int kThreads = 512;                 // eight waves
+constexpr uint32_t kTileLds = kT * kD * 2;    // 32 KB per K or V tile buffer
+
+struct PPState {
+  f32x16 o[4];       // O^T [4 x 32 dims][32 queries]
+  f32x16 s[2];       // S^T of the group's 64 keys of the current tile: two 32-key blocks
+  bf16x8 p[4];       // P^T operands of the previous tile: four 16-key steps
+  float m, l;
+};
+
+// MFMA phase of group G: PV of the previous tile (buffer pbuf) and S of the
+// current tile (buffer sbuf).
+template <int G, bool DO_PV, bool DO_S>
+__device__ __forceinline__ void pp_mfma(PPState& st, const bf16x8 (&qf)[8], const uint32_t (&rd)[8],
+                                        const uint8_t* lds_k, const uint8_t* lds_v, int pbuf, int sbuf) {
+  if constexpr (DO_PV) {
+    const uint8_t* vbase = lds_v + pbuf * kTileLds;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint4*>(vbase + rd[4 * G + j] + mb * 8192));
+        st.o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, st.p[j], st.o[mb], 0, 0, 0);
+      }
+  }
+  if constexpr (DO_S) {
+    const uint8_t* kbase = lds_k + sbuf * kTileLds + G * 64 * 256;
+    st.s[0] = f32x16{};
+    st.s[1] = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(kbase + rd[ks] + kb * 8192));
+        st.s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st.s[kb], 0, 0, 0);
+      }
+  }
+  // Keep a bounded number of operand reads in flight: six ahead, then one
+  // read per MFMA (bounds register use; hides LDS latency).
+  constexpr int kN = (DO_PV ? 16 : 0) + (DO_S ? 16 : 0);
+  constexpr int kAhead = 6;
+  __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+  for (int i = 0; i < kN - kAhead; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+}
+
+// VALU phase: softmax of the group's 64 keys of the current tile; `valid` is
+// the number of valid keys among them (0..64).
+__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float c2, float lazy_raw) {
+  if (valid < 64) {
+    // key kb*32 + 8*(e>>2) + 4*hl + (e&3) is padding when it is >= valid
+    const int vl = valid - 4 * hl;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (kb * 32 + 8 * (e >> 2) + (e & 3) >= vl) st.s[kb][e] = -INFINITY;
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st.s[kb][e]);
+  mx = pair_max(mx);
+  if (__ballot(mx > st.m + lazy_raw) != 0) {   // wave-uniform, rare after the first tile
+    const float mnew = fmaxf(st.m, mx);
+    const float alpha = (st.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((st.m - mnew) * c2);
+    st.m = mnew;
+    st.l *= alpha;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) st.o[mb] *= alpha;
+  }
+  const float mb2 = (st.m == -INFINITY) ? 0.f : st.m * c2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float rs = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int kb = j >> 1, hh = j & 1;
+    bf16x2 pr[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(st.s[kb][8 * hh + 2 * e], c2, -mb2));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(st.s[kb][8 * hh + 2 * e + 1], c2, -mb2));
+      pr[e] = bf16x2{(__bf16)p0, (__bf16)p1};
+      rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], ones, rs, false);
+    }
+    st.p[j] = __builtin_shufflevector(__builtin_shufflevector(pr[0], pr[1], 0, 1, 2, 3),
+                                      __builtin_shufflevector(pr[2], pr[3], 0, 1, 2, 3),
+                                      0, 1, 2, 3, 4, 5, 6, 7);
+  }
+  st.l += pair_sum(rs);
+}
+
+__global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
+  __shared__ uint4 sK[2][kT * 16];   // two K tiles: 128 key rows x 16 chunks
+  __shared__ uint4 sV[2][kD * 16];   // two V^T tiles: 128 dim rows x 16 chunks
+
+  const int row = blockIdx.x;
+  const int qt = row % a.NT;
+  const int bh = row / a.NT;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;          // 0: keys 0..63, 1: keys 64..127
+  const int qw = wave & 3;            // query block of the wave
+  const int lane = tid & 63;
+  const int hl = lane >> 5;
+  const int ln = lane & 31;
+  const int qrow = qt * kT + qw * 32 + ln;
+  const bool qvalid = qrow < a.L;
+
+  // Q^T as the B operand: lane holds query ln, dims 16*ks + 8*hl .. +8.
+  bf16x8 qf[8];
+  {
+    const uint16_t* qp = a.q + ((size_t(b) * a.L + (qvalid ? qrow : 0)) * a.H + h) * kD + 8 * hl;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (qvalid) u = *reinterpret_cast<const uint4*>(qp + 16 * ks);
+      qf[ks] = as_bf16x8(u);
+    }
+  }
+  // Q is in registers before any page copy is issued, so that the only
+  // vector-memory operations in flight inside the loop are page copies.
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+
+  // Copy i of wave w fills LDS chunks [64*(8i + w), +64) of a tile buffer; row
+  // r chunk c is stored at r*16 + (c ^ (r & 15)) (K rows = keys, V^T rows =
+  // dims).  Operand reads: row ln of a 32-row block, logical chunk 2j + hl.
+  uint32_t dma[4], rd[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int p = (8 * i + wave) * 64 + lane;
+    const int r = p >> 4, cs = p & 15;
+    dma[i] = uint32_t(r * 256 + ((cs ^ (r & 15)) * 16));
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) rd[j] = uint32_t(ln * 256 + (((2 * j + hl) ^ (ln & 15)) * 16));
+  const uint32_t k_lds = lds_addr(&sK[0][0]) + uint32_t(wave) * 1024u;
+  const uint32_t v_lds = lds_addr(&sV[0][0]) + uint32_t(wave) * 1024u;
+  const uint8_t* lds_k = reinterpret_cast<const uint8_t*>(&sK[0][0]);
+  const uint8_t* lds_v = reinterpret_cast<const uint8_t*>(&sV[0][0]);
+
+  const size_t pbytes = page_bytes(kT, kD);
+  const uint8_t* head_pages = a.pool + (size_t(b) * a.H + h) * a.NT * pbytes;
+  const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
+  const int count = ((const const_i32*)a.counts)[row];
+  const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
+  const float c2 = a.scale_log2;
+  const float lazy_raw = kLazyLog2 / fabsf(c2);
+
+  // Page of list entry n and its valid keys.  An entry naming a tile outside
+  // the window (stale lists) reads a page of this head and counts no key.
+  auto page_of = [&](int n, int& valid) {
+    const int j = list[n];
+    if (unsigned(j) >= unsigned(a.nk)) {
+      valid = 0;
+      return head_pages + size_t(a.slot_of[0]) * slot_stride;
+    }
+    const int pos = j / a.NT;
+    const int t = j - pos * a.NT;
+    valid = (t == a.NT - 1) ? a.tail : kT;
+    return head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
+  };
+  auto issue_k = [&](int n) {
+    int v;
+    const uint8_t* src = page_of(n, v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(src, dma[i], k_lds + uint32_t(n & 1) * kTileLds + uint32_t(i) * 8192u);
+  };
+  auto issue_v = [&](int n) {
+    int v;
+    const uint8_t* src = page_of(n, v) + size_t(kT) * kD * 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(src, dma[i], v_lds + uint32_t(n & 1) * kTileLds + uint32_t(i) * 8192u);
+  };
+  auto group_valid = [&](int n) {
+    int v;
+    page_of(n, v);
+    return min(max(v - 64 * grp, 0), 64);
+  };
+  auto sync = [&]() {
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    __builtin_amdgcn_s_barrier();
+  };
+
+  PPState st;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) st.o[mb] = f32x16{};
+  st.m = -INFINITY;
+  st.l = 0.f;
+
+  const int N = count;
+  if (N > 0) {
+    // prologue: K tile 0, V tile 0, K tile 1; phase 0 needs K tile 0 only
+    issue_k(0);
+    issue_v(0);
+    if (N > 1) {
+      issue_k(1);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
+    } else {
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(4));
+    }
+    __builtin_amdgcn_s_barrier();
+
+    // Phase pair m: phase 2m (A: MFMA, B: softmax), phase 2m+1 (A: softmax,
+    // B: MFMA).  m = 0 and m = N are peeled so that the steady-state body is
+    // a single variant.  Each group runs its own copy of the phase sequence;
+    // both copies pass the same barriers in the same order.
+    auto top = [&](int m) {
+      // copies issued at phase 2m-2 (K tile m, V tile m-1) have landed; the
+      // buffers of K tile m-1 and V tile m-2 were last read at phase 2m-1
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+      __builtin_amdgcn_s_barrier();
+      if (m + 1 < N) issue_k(m + 1);
+      if (m < N) issue_v(m);
+    };
+    auto mfma_phase = [&](auto G, auto do_pv, auto do_s, int m) {
+      __builtin_amdgcn_s_setprio(1);
+      pp_mfma<decltype(G)::value, decltype(do_pv)::value, decltype(do_s)::value>(
+          st, qf, rd, lds_k, lds_v, (m - 1) & 1, m & 1);
+      __builtin_amdgcn_s_setprio(0);
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using T = std::true_type;
+    using F = std::false_type;
+    if (grp == 0) {
+      mfma_phase(I0{}, F{}, T{}, 0);
+      sync();
+      pp_softmax(st, group_valid(0), hl, c2, lazy_raw);
+      for (int m = 1; m < N; ++m) {
+        top(m);
+        mfma_phase(I0{}, T{}, T{}, m);
+        sync();
+        pp_softmax(st, group_valid(m), hl, c2, lazy_raw);
+      }
+      top(N);
+      mfma_phase(I0{}, T{}, F{}, N);
+      sync();
+    } else {
+      sync();
+      mfma_phase(I1{}, F{}, T{}, 0);
+      for (int m = 1; m < N; ++m) {
+        top(m);
+        pp_softmax(st, group_valid(m - 1), hl, c2, lazy_raw);
+        sync();
+        mfma_phase(I1{}, T{}, T{}, m);
+      }
+      top(N);
+      pp_softmax(st, group_valid(N - 1), hl, c2, lazy_raw);
+      sync();
+      mfma_phase(I1{}, T{}, F{}, N);
+    }
+  }
+
+  // ---- merge the two key halves: group B hands (m, l, O) to group A ----
+  sync();   // every operand read of the loop is done; the K buffers are free
+  float* xo = reinterpret_cast<float*>(&sK[0][0]);   // [4 waves][4 blocks][16][64 lanes]: 64 KB
+  float* xm = reinterpret_cast<float*>(&sV[0][0]);   // [2][4 waves][64 lanes]: m, then l
+  if (grp == 1) {
+    xm[qw * 64 + lane] = st.m;
+    xm[256 + qw * 64 + lane] = st.l;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) xo[((qw * 4 + mb) * 16 + e) * 64 + lane] = st.o[mb][e];
+  }
+  sync();
+  if (grp == 0) {
+    const float mB = xm[qw * 64 + lane];
+    const float lB = xm[256 + qw * 64 + lane];
+    const float mm = fmaxf(st.m, mB);
+    const float fa = (st.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((st.m - mm) * c2);
+    const float fb = (mB == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((mB - mm) * c2);
+    const float l = st.l * fa + lB * fb;
+    if (qvalid) {
+      const float inv = (l > 0.f) ? 1.f / l : 0.f;
+      const float wa = fa * inv, wb = fb * inv;
+      uint16_t* op = a.o + ((size_t(b) * a.L + qrow) * a.H + h) * kD;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d0 = mb * 32 + 8 * i + 4 * hl;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[e] = st.o[mb][4 * i + e] * wa + xo[((qw * 4 + mb) * 16 + 4 * i + e) * 64 + lane] * wb;
+          uint2 w;
+          w.x = pack_bf16x2(v[0], v[1]);
+          w.y = pack_bf16x2(v[2], v[3]);
+          *reinterpret_cast<uint2*>(op + d0) = w;
+        }
+      if (a.lse != nullptr && hl == 0)
+        a.lse[(size_t(b) * a.H + h) * a.L + qrow] = (l > 0.f) ? mm * a.scale + logf(l) : -INFINITY;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream) {
+  const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
+  attn_fwd_pp_kernel<<<blocks, kThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace uf

@@ -6,7 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/uf.h"
+#include "uf.h"
 
 namespace uf {
 
@@ -55,6 +55,12 @@ struct AttnArgs {
   float scale_log2;       // scale * log2(e)
   int32_t slot_of[UF_MAX_CHUNKS];  // slot of each logical position
 };
-hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t128_w32(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream);
+
+inline hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
+  return a.T == 128 ? launch_attn_fwd_t128_pp(a, stream) : launch_attn_fwd_t64(a, stream);
+}
 
 }  // namespace uf
