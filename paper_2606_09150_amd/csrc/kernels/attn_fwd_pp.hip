@@ -27,9 +27,14 @@
 //
 // Memory.  Whole tiles are copied HBM -> LDS by direct global_load_lds
 // (16 bytes per lane, XOR-swizzled 16-byte chunks, conflict-free operand
-// reads) into two K and two V tile buffers (128 KB).  At the start of phase
-// 2m the K tile m+1 and the V tile m are requested; each is first read two
-// phases later.
+// reads) into two K and three V tile buffers (160 KB, all of the CU's LDS).
+// The copies are issued by the group that is in its softmax phase, spread
+// through its VALU work (which has slack against the other group's MFMA
+// phase), so the MFMA phases carry no copy instructions and the per-CU memory
+// pipeline is fed evenly: group B requests K tile m+1 during phase 2m (first
+// read at phase 2m+2), group A requests V tile m+1 during phase 2m+1 (first
+// read at phase 2m+4).  A buffer is refilled only after a barrier that
+// follows its last read.
 //
 // Softmax in base 2 with scale*log2(e) folded into one FMA; the running max is
 // raised lazily (only when it grows by more than 2^8); row sums add the
@@ -96,7 +101,16 @@ __device__ __forceinline__ void pp_mfma(PPState& st, const bf16x8 (&qf)[8], cons
 
 // VALU phase: softmax of the group's 64 keys of the current tile; `valid` is
 // the number of valid keys among them (0..64).
-__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float c2, float lazy_raw) {
+// Copies issued during a softmax phase: eight 16-byte-per-lane copies of the
+// wave (copy i fills chunks [64*(4i + q), +64) of the target tile buffer).
+struct CopyJob {
+  const uint8_t* src;   // uniform page block
+  uint32_t lds;         // LDS byte address of the target buffer plus 1 KB * q
+  bool on;
+};
+
+__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float c2, float lazy_raw,
+                                           const CopyJob& cj, const uint32_t (&dma)[8]) {
   if (valid < 64) {
     // key kb*32 + 8*(e>>2) + 4*hl + (e&3) is padding when it is >= valid
     const int vl = valid - 4 * hl;
@@ -105,6 +119,10 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float
 #pragma unroll
       for (int e = 0; e < 16; ++e)
         if (kb * 32 + 8 * (e >> 2) + (e & 3) >= vl) st.s[kb][e] = -INFINITY;
+  }
+  if (cj.on) {
+    dma16(cj.src, dma[0], cj.lds);
+    dma16(cj.src, dma[1], cj.lds + 4096u);
   }
   float mx = -INFINITY;
 #pragma unroll
@@ -126,6 +144,10 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int kb = j >> 1, hh = j & 1;
+    if (cj.on && j < 3) {
+      dma16(cj.src, dma[2 + 2 * j], cj.lds + uint32_t(2 + 2 * j) * 4096u);
+      dma16(cj.src, dma[3 + 2 * j], cj.lds + uint32_t(3 + 2 * j) * 4096u);
+    }
     bf16x2 pr[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -143,7 +165,7 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float
 
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   __shared__ uint4 sK[2][kT * 16];   // two K tiles: 128 key rows x 16 chunks
-  __shared__ uint4 sV[2][kD * 16];   // two V^T tiles: 128 dim rows x 16 chunks
+  __shared__ uint4 sV[3][kD * 16];   // three V^T tiles: 128 dim rows x 16 chunks
 
   const int row = blockIdx.x;
   const int qt = row % a.NT;
@@ -175,20 +197,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   // vector-memory operations in flight inside the loop are page copies.
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
-  // Copy i of wave w fills LDS chunks [64*(8i + w), +64) of a tile buffer; row
+  // Copy i of wave q of a group fills LDS chunks [64*(4i + q), +64) of a tile buffer; row
   // r chunk c is stored at r*16 + (c ^ (r & 15)) (K rows = keys, V^T rows =
   // dims).  Operand reads: row ln of a 32-row block, logical chunk 2j + hl.
-  uint32_t dma[4], rd[8];
+  uint32_t dma[8], rd[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int p = (8 * i + wave) * 64 + lane;
+  for (int i = 0; i < 8; ++i) {
+    const int p = (4 * i + qw) * 64 + lane;
     const int r = p >> 4, cs = p & 15;
     dma[i] = uint32_t(r * 256 + ((cs ^ (r & 15)) * 16));
   }
 #pragma unroll
   for (int j = 0; j < 8; ++j) rd[j] = uint32_t(ln * 256 + (((2 * j + hl) ^ (ln & 15)) * 16));
-  const uint32_t k_lds = lds_addr(&sK[0][0]) + uint32_t(wave) * 1024u;
-  const uint32_t v_lds = lds_addr(&sV[0][0]) + uint32_t(wave) * 1024u;
+  const uint32_t k_lds = lds_addr(&sK[0][0]) + uint32_t(qw) * 1024u;
+  const uint32_t v_lds = lds_addr(&sV[0][0]) + uint32_t(qw) * 1024u;
   const uint8_t* lds_k = reinterpret_cast<const uint8_t*>(&sK[0][0]);
   const uint8_t* lds_v = reinterpret_cast<const uint8_t*>(&sV[0][0]);
 
@@ -196,6 +218,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   const uint8_t* head_pages = a.pool + (size_t(b) * a.H + h) * a.NT * pbytes;
   const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
   const int count = ((const const_i32*)a.counts)[row];
+  const int N = count;
   const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
   const float c2 = a.scale_log2;
   const float lazy_raw = kLazyLog2 / fabsf(c2);
@@ -213,17 +236,26 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     valid = (t == a.NT - 1) ? a.tail : kT;
     return head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
   };
-  auto issue_k = [&](int n) {
+  // Copy jobs: K tile n into K buffer n % 2, V tile n into V buffer n % 3.
+  auto kjob = [&](int n) {
+    CopyJob c;
+    c.on = n < N;
     int v;
-    const uint8_t* src = page_of(n, v);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(src, dma[i], k_lds + uint32_t(n & 1) * kTileLds + uint32_t(i) * 8192u);
+    c.src = c.on ? page_of(n, v) : head_pages;
+    c.lds = k_lds + uint32_t(n & 1) * kTileLds;
+    return c;
   };
-  auto issue_v = [&](int n) {
+  auto vjob = [&](int n) {
+    CopyJob c;
+    c.on = n < N;
     int v;
-    const uint8_t* src = page_of(n, v) + size_t(kT) * kD * 2;
+    c.src = (c.on ? page_of(n, v) : head_pages) + size_t(kT) * kD * 2;
+    c.lds = v_lds + uint32_t(n % 3) * kTileLds;
+    return c;
+  };
+  auto issue = [&](const CopyJob& c) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(src, dma[i], v_lds + uint32_t(n & 1) * kTileLds + uint32_t(i) * 8192u);
+    for (int i = 0; i < 8; ++i) dma16(c.src, dma[i], c.lds + uint32_t(i) * 4096u);
   };
   auto group_valid = [&](int n) {
     int v;
@@ -241,16 +273,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   st.m = -INFINITY;
   st.l = 0.f;
 
-  const int N = count;
   if (N > 0) {
-    // prologue: K tile 0, V tile 0, K tile 1; phase 0 needs K tile 0 only
-    issue_k(0);
-    issue_v(0);
-    if (N > 1) {
-      issue_k(1);
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
+    // prologue: B copies K tile 0 (needed by phase 0), A copies V tile 0
+    if (grp == 1) {
+      issue(kjob(0));
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     } else {
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(4));
+      issue(vjob(0));
     }
     __builtin_amdgcn_s_barrier();
 
@@ -258,19 +287,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     // B: MFMA).  m = 0 and m = N are peeled so that the steady-state body is
     // a single variant.  Each group runs its own copy of the phase sequence;
     // both copies pass the same barriers in the same order.
+    // top(m): barrier ahead of phase 2m.  B's K tile m (copied in phase
+    // 2m-2) has landed; A's V tile m-1 (copied in phase 2m-3) has landed
+    // while its V tile m (copied in phase 2m-1) may still be in flight.
     auto top = [&](int m) {
-      // copies issued at phase 2m-2 (K tile m, V tile m-1) have landed; the
-      // buffers of K tile m-1 and V tile m-2 were last read at phase 2m-1
       __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+      if (grp == 0 && m < N)
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
+      else
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
       __builtin_amdgcn_s_barrier();
-      if (m + 1 < N) issue_k(m + 1);
-      if (m < N) issue_v(m);
     };
+    const CopyJob none = {head_pages, 0u, false};
     auto mfma_phase = [&](auto G, auto do_pv, auto do_s, int m) {
       __builtin_amdgcn_s_setprio(1);
       pp_mfma<decltype(G)::value, decltype(do_pv)::value, decltype(do_s)::value>(
-          st, qf, rd, lds_k, lds_v, (m - 1) & 1, m & 1);
+          st, qf, rd, lds_k, lds_v, (m + 2) % 3, m & 1);
       __builtin_amdgcn_s_setprio(0);
     };
     using I0 = std::integral_constant<int, 0>;
@@ -280,27 +312,28 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     if (grp == 0) {
       mfma_phase(I0{}, F{}, T{}, 0);
       sync();
-      pp_softmax(st, group_valid(0), hl, c2, lazy_raw);
+      pp_softmax(st, group_valid(0), hl, c2, lazy_raw, vjob(1), dma);
       for (int m = 1; m < N; ++m) {
         top(m);
         mfma_phase(I0{}, T{}, T{}, m);
         sync();
-        pp_softmax(st, group_valid(m), hl, c2, lazy_raw);
+        pp_softmax(st, group_valid(m), hl, c2, lazy_raw, vjob(m + 1), dma);
       }
       top(N);
       mfma_phase(I0{}, T{}, F{}, N);
       sync();
     } else {
+      issue(kjob(1));   // phase 0: B has no softmax work yet
       sync();
       mfma_phase(I1{}, F{}, T{}, 0);
       for (int m = 1; m < N; ++m) {
         top(m);
-        pp_softmax(st, group_valid(m - 1), hl, c2, lazy_raw);
+        pp_softmax(st, group_valid(m - 1), hl, c2, lazy_raw, kjob(m + 1), dma);
         sync();
         mfma_phase(I1{}, T{}, T{}, m);
       }
       top(N);
-      pp_softmax(st, group_valid(N - 1), hl, c2, lazy_raw);
+      pp_softmax(st, group_valid(N - 1), hl, c2, lazy_raw, none, dma);
       sync();
       mfma_phase(I1{}, T{}, F{}, N);
     }
@@ -309,7 +342,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   // ---- merge the two key halves: group B hands (m, l, O) to group A ----
   sync();   // every operand read of the loop is done; the K buffers are free
   float* xo = reinterpret_cast<float*>(&sK[0][0]);   // [4 waves][4 blocks][16][64 lanes]: 64 KB
-  float* xm = reinterpret_cast<float*>(&sV[0][0]);   // [2][4 waves][64 lanes]: m, then l
+  float* xm = reinterpret_cast<float*>(&sV[0][0]);   // [2][4 waves][64 lanes]: m, then l (V buffer 0)
   if (grp == 1) {
     xm[qw * 64 + lane] = st.m;
     xm[256 + qw * 64 + lane] = st.l;
