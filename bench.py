@@ -34,6 +34,43 @@ METRIC = "ms per chunk + effective TFLOP/s (kept tiles) of sparse causal attn, 1
 MFMA_BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense
 HBM_PEAK_GBPS = 8000.0
 D = 128
+# Measured HBM traffic of the attention kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
+# scaled by a plain copy of known size), valid only for the kernel sources it was
+# measured on: their SHA-256 is recorded beside the figure.
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_fwd_pp_1k_traffic.md")
+ATTN_SOURCES = ("paper_2606_09150_amd/csrc/kernels/attn_fwd_pp.hip",
+                "paper_2606_09150_amd/csrc/kernels/attn_common.h",
+                "paper_2606_09150_amd/csrc/launch.h")
+
+
+def attn_sources_sha256():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in ATTN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config):
+    """Bytes per attention launch from the committed counter summary, or None when the
+    summary is missing, covers another workload, or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_PROFILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].split(": ", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    try:
+        if fields["workload"] != config or fields["kernel_sources_sha256"] != attn_sources_sha256():
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def _flops_of_lists(win, lists, nt, tail, T):
@@ -161,6 +198,11 @@ def cpu_baseline(wl, state, target_s):
                 f += vq * (tail if j % nt == nt - 1 else T)
         return f * 4 * D
 
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:   # threadpoolctl missing: report the affinity set
+        threads = len(os.sched_getaffinity(0))
     t0 = time.perf_counter()
     oracle.sparse_causal_attention(ring, q, bits, T, scale, qtiles=[0])
     one = time.perf_counter() - t0
@@ -172,7 +214,7 @@ def cpu_baseline(wl, state, target_s):
     return {
         "value": kept_flops(tiles) / sec / 1e12,
         "unit": "TFLOP/s",
-        "cores": len(os.sched_getaffinity(0)),
+        "cores": threads,
         "kind": "oracle",
         "sample": f"{wl.name}: head 0, query tiles 1..{n} of {nt} ({n * T} queries x {L * info.n_live} keys, "
                   f"float64 numpy masked-dense), {sec:.1f} s; throughput in kept-tile FLOP/s",
@@ -240,7 +282,7 @@ def main():
         "peak": MFMA_BF16_PEAK_TFLOPS,
         "unit": "TFLOP/s",
         "frac": res["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS,
-        "traffic": None,
+        "traffic": measured_traffic(wl.name),
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, state, args.cpu_seconds)
