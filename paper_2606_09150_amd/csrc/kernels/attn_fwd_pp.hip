@@ -36,9 +36,17 @@
 // read at phase 2m+4).  A buffer is refilled only after a barrier that
 // follows its last read.
 //
-// Softmax in base 2 with scale*log2(e) folded into one FMA; the running max is
-// raised lazily (only when it grows by more than 2^8); row sums add the
-// bf16-rounded weights (v_dot2_f32_bf16).
+// Softmax in base 2.  Q is scaled by scale*log2(e) once, when it is loaded
+// (rounded to bf16, as an input-precision scaling of Q), and every S
+// accumulator starts at -m, the lane's current offset, so the MFMA result is
+// already the exponent: a weight costs one exp2.  The offset is not the exact
+// running max: it is raised only when the weights it gives grow too large,
+// which the row sums (bf16-rounded weights added with v_dot2_f32_bf16)
+// reveal without a max reduction.  Then, and on a lane's first valid key, the
+// exact max is taken, O and l are rescaled and the tile's weights are
+// recomputed.  Weights stay below 2^12 before normalisation, far from
+// overflow, and normalisation by l makes the result independent of the
+// offset up to rounding.
 #include "attn_common.h"
 
 #include <type_traits>
@@ -54,10 +62,15 @@ constexpr uint32_t kTileLds = kT * kD * 2;    // 32 KB per K or V tile buffer
 
 struct PPState {
   f32x16 o[4];       // O^T [4 x 32 dims][32 queries]
-  f32x16 s[2];       // S^T of the group's 64 keys of the current tile: two 32-key blocks
+  f32x16 s[2];       // S^T - m of the group's 64 keys of the current tile, base-2 units
   bf16x8 p[4];       // P^T operands of the previous tile: four 16-key steps
-  float m, l;
+  f32x16 negm;       // -m broadcast (0 while m is -inf): initial value of S accumulators
+  float m;           // offset (base-2 units), -inf until the lane's first valid key
+  float l;           // this lane's share of the row sum; the partner lane holds the rest
 };
+
+// Row-sum bound of one lane's 32 weights above which the offset is raised.
+constexpr float kSumBound = 4096.0f;
 
 // MFMA phase of group G: PV of the previous tile (buffer pbuf) and S of the
 // current tile (buffer sbuf).
@@ -76,14 +89,12 @@ __device__ __forceinline__ void pp_mfma(PPState& st, const bf16x8 (&qf)[8], cons
   }
   if constexpr (DO_S) {
     const uint8_t* kbase = lds_k + sbuf * kTileLds + G * 64 * 256;
-    st.s[0] = f32x16{};
-    st.s[1] = f32x16{};
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(kbase + rd[ks] + kb * 8192));
-        st.s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st.s[kb], 0, 0, 0);
+        st.s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], ks == 0 ? st.negm : st.s[kb], 0, 0, 0);
       }
   }
   // Keep a bounded number of operand reads in flight: six ahead, then one
@@ -99,8 +110,6 @@ __device__ __forceinline__ void pp_mfma(PPState& st, const bf16x8 (&qf)[8], cons
   __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
 }
 
-// VALU phase: softmax of the group's 64 keys of the current tile; `valid` is
-// the number of valid keys among them (0..64).
 // Copies issued during a softmax phase: eight 16-byte-per-lane copies of the
 // wave (copy i fills chunks [64*(4i + q), +64) of the target tile buffer).
 struct CopyJob {
@@ -109,8 +118,43 @@ struct CopyJob {
   bool on;
 };
 
-__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float c2, float lazy_raw,
-                                           const CopyJob& cj, const uint32_t (&dma)[8]) {
+// Weights exp2(s - sh) of the group's 64 keys as P^T operands; returns the
+// lane's sum of the bf16-rounded weights.  The copies of `cj` are spread
+// through the work when `copies` is set.
+template <bool SHIFT>
+__device__ __forceinline__ float pp_weights(PPState& st, float sh, const CopyJob& cj, const uint32_t (&dma)[8],
+                                            bool copies) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float rs = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int kb = j >> 1, hh = j & 1;
+    if (copies && cj.on) {
+      dma16(cj.src, dma[2 * j], cj.lds + uint32_t(2 * j) * 4096u);
+      dma16(cj.src, dma[2 * j + 1], cj.lds + uint32_t(2 * j + 1) * 4096u);
+    }
+    bf16x2 pr[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float x0 = st.s[kb][8 * hh + 2 * e], x1 = st.s[kb][8 * hh + 2 * e + 1];
+      if constexpr (SHIFT) {
+        x0 -= sh;
+        x1 -= sh;
+      }
+      pr[e] = bf16x2{(__bf16)__builtin_amdgcn_exp2f(x0), (__bf16)__builtin_amdgcn_exp2f(x1)};
+      rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], ones, rs, false);
+    }
+    st.p[j] = __builtin_shufflevector(__builtin_shufflevector(pr[0], pr[1], 0, 1, 2, 3),
+                                      __builtin_shufflevector(pr[2], pr[3], 0, 1, 2, 3),
+                                      0, 1, 2, 3, 4, 5, 6, 7);
+  }
+  return rs;
+}
+
+// VALU phase: weights of the group's 64 keys of the current tile; `valid` is
+// the number of valid keys among them (0..64).
+__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, const CopyJob& cj,
+                                           const uint32_t (&dma)[8]) {
   if (valid < 64) {
     // key kb*32 + 8*(e>>2) + 4*hl + (e&3) is padding when it is >= valid
     const int vl = valid - 4 * hl;
@@ -120,47 +164,34 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float
       for (int e = 0; e < 16; ++e)
         if (kb * 32 + 8 * (e >> 2) + (e & 3) >= vl) st.s[kb][e] = -INFINITY;
   }
-  if (cj.on) {
-    dma16(cj.src, dma[0], cj.lds);
-    dma16(cj.src, dma[1], cj.lds + 4096u);
-  }
-  float mx = -INFINITY;
+  float rs = pp_weights<false>(st, 0.f, cj, dma, true);
+  // wave-uniform: some lane has no offset yet, or its weights grew too large
+  if (__ballot(!(st.m > -INFINITY) || rs > kSumBound) != 0) {
+    float mx = -INFINITY;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st.s[kb][e]);
-  mx = pair_max(mx);
-  if (__ballot(mx > st.m + lazy_raw) != 0) {   // wave-uniform, rare after the first tile
-    const float mnew = fmaxf(st.m, mx);
-    const float alpha = (st.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((st.m - mnew) * c2);
-    st.m = mnew;
-    st.l *= alpha;
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st.s[kb][e]);
+    mx = pair_max(mx);   // max of s - m over the query's valid keys of this tile
+    float sh;
+    if (st.m > -INFINITY) {
+      sh = fmaxf(mx, 0.f);
+      const float alpha = __builtin_amdgcn_exp2f(-sh);
+      st.m += sh;
+      st.l *= alpha;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) st.o[mb] *= alpha;
-  }
-  const float mb2 = (st.m == -INFINITY) ? 0.f : st.m * c2;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  float rs = 0.f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int kb = j >> 1, hh = j & 1;
-    if (cj.on && j < 3) {
-      dma16(cj.src, dma[2 + 2 * j], cj.lds + uint32_t(2 + 2 * j) * 4096u);
-      dma16(cj.src, dma[3 + 2 * j], cj.lds + uint32_t(3 + 2 * j) * 4096u);
+      for (int mb = 0; mb < 4; ++mb) st.o[mb] *= alpha;
+    } else {
+      // first valid key of the lane (s holds the raw exponents): offset = max
+      sh = (mx > -INFINITY) ? mx : 0.f;
+      st.m = mx;
     }
-    bf16x2 pr[4];
+    const float nm = (st.m > -INFINITY) ? -st.m : 0.f;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(st.s[kb][8 * hh + 2 * e], c2, -mb2));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(st.s[kb][8 * hh + 2 * e + 1], c2, -mb2));
-      pr[e] = bf16x2{(__bf16)p0, (__bf16)p1};
-      rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], ones, rs, false);
-    }
-    st.p[j] = __builtin_shufflevector(__builtin_shufflevector(pr[0], pr[1], 0, 1, 2, 3),
-                                      __builtin_shufflevector(pr[2], pr[3], 0, 1, 2, 3),
-                                      0, 1, 2, 3, 4, 5, 6, 7);
+    for (int e = 0; e < 16; ++e) st.negm[e] = nm;
+    rs = pp_weights<true>(st, sh, cj, dma, false);
   }
-  st.l += pair_sum(rs);
+  st.l += rs;
 }
 
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
@@ -190,7 +221,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     for (int ks = 0; ks < 8; ++ks) {
       uint4 u = make_uint4(0, 0, 0, 0);
       if (qvalid) u = *reinterpret_cast<const uint4*>(qp + 16 * ks);
-      qf[ks] = as_bf16x8(u);
+      const bf16x8 raw = as_bf16x8(u);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[ks][e] = (__bf16)(float(raw[e]) * a.scale_log2);
     }
   }
   // Q is in registers before any page copy is issued, so that the only
@@ -220,8 +253,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   const int count = ((const const_i32*)a.counts)[row];
   const int N = count;
   const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
-  const float c2 = a.scale_log2;
-  const float lazy_raw = kLazyLog2 / fabsf(c2);
 
   // Page of list entry n and its valid keys.  An entry naming a tile outside
   // the window (stale lists) reads a page of this head and counts no key.
@@ -270,6 +301,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   PPState st;
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) st.o[mb] = f32x16{};
+  st.negm = f32x16{};
   st.m = -INFINITY;
   st.l = 0.f;
 
@@ -312,12 +344,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     if (grp == 0) {
       mfma_phase(I0{}, F{}, T{}, 0);
       sync();
-      pp_softmax(st, group_valid(0), hl, c2, lazy_raw, vjob(1), dma);
+      pp_softmax(st, group_valid(0), hl, vjob(1), dma);
       for (int m = 1; m < N; ++m) {
         top(m);
         mfma_phase(I0{}, T{}, T{}, m);
         sync();
-        pp_softmax(st, group_valid(m), hl, c2, lazy_raw, vjob(m + 1), dma);
+        pp_softmax(st, group_valid(m), hl, vjob(m + 1), dma);
       }
       top(N);
       mfma_phase(I0{}, T{}, F{}, N);
@@ -328,18 +360,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
       mfma_phase(I1{}, F{}, T{}, 0);
       for (int m = 1; m < N; ++m) {
         top(m);
-        pp_softmax(st, group_valid(m - 1), hl, c2, lazy_raw, kjob(m + 1), dma);
+        pp_softmax(st, group_valid(m - 1), hl, kjob(m + 1), dma);
         sync();
         mfma_phase(I1{}, T{}, T{}, m);
       }
       top(N);
-      pp_softmax(st, group_valid(N - 1), hl, c2, lazy_raw, none, dma);
+      pp_softmax(st, group_valid(N - 1), hl, none, dma);
       sync();
       mfma_phase(I1{}, T{}, F{}, N);
     }
   }
 
   // ---- merge the two key halves: group B hands (m, l, O) to group A ----
+  st.l = pair_sum(st.l);
   sync();   // every operand read of the loop is done; the K buffers are free
   float* xo = reinterpret_cast<float*>(&sK[0][0]);   // [4 waves][4 blocks][16][64 lanes]: 64 KB
   float* xm = reinterpret_cast<float*>(&sV[0][0]);   // [2][4 waves][64 lanes]: m, then l (V buffer 0)
@@ -356,8 +389,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     const float mB = xm[qw * 64 + lane];
     const float lB = xm[256 + qw * 64 + lane];
     const float mm = fmaxf(st.m, mB);
-    const float fa = (st.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((st.m - mm) * c2);
-    const float fb = (mB == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f((mB - mm) * c2);
+    const float fa = (st.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(st.m - mm);
+    const float fb = (mB == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mB - mm);
     const float l = st.l * fa + lB * fb;
     if (qvalid) {
       const float inv = (l > 0.f) ? 1.f / l : 0.f;
@@ -378,7 +411,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
           *reinterpret_cast<uint2*>(op + d0) = w;
         }
       if (a.lse != nullptr && hl == 0)
-        a.lse[(size_t(b) * a.H + h) * a.L + qrow] = (l > 0.f) ? mm * a.scale + logf(l) : -INFINITY;
+        a.lse[(size_t(b) * a.H + h) * a.L + qrow] = (l > 0.f) ? (mm + log2f(l)) * 0.69314718055994531f : -INFINITY;
     }
   }
 }
