@@ -177,8 +177,10 @@ int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists
  * A row with no kept tile gives O = 0 and LSE = -inf.  q, o: [B, L, H, D] bf16,
  * 16-byte aligned; lse: [B, H, L] fp32 or NULL; d_lists as built by
  * uf_build_tile_lists for the current window (entries naming a tile outside
- * the window are skipped).  Computes in fp32 with bf16 MFMA products; O is
- * rounded to nearest even.  Errors: UF_ERR_ARG, UF_ERR_EMPTY, UF_ERR_HIP. */
+ * the window are skipped).  scale must be positive and finite, with
+ * scale*log2(e) a normal float (else UF_ERR_ARG).  Computes in fp32 with bf16
+ * MFMA products; O is rounded to nearest even.  Errors: UF_ERR_ARG,
+ * UF_ERR_EMPTY, UF_ERR_HIP. */
 int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists,
                               float scale, void* d_o, float* d_lse, void* stream);
 

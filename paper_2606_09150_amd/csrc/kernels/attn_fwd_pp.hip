@@ -36,17 +36,17 @@
 // read at phase 2m+4).  A buffer is refilled only after a barrier that
 // follows its last read.
 //
-// Softmax in base 2.  Q is scaled by scale*log2(e) once, when it is loaded
-// (rounded to bf16, as an input-precision scaling of Q), and every S
-// accumulator starts at -m, the lane's current offset, so the MFMA result is
-// already the exponent: a weight costs one exp2.  The offset is not the exact
-// running max: it is raised only when the weights it gives grow too large,
-// which the row sums (bf16-rounded weights added with v_dot2_f32_bf16)
-// reveal without a max reduction.  Then, and on a lane's first valid key, the
-// exact max is taken, O and l are rescaled and the tile's weights are
-// recomputed.  Weights stay below 2^12 before normalisation, far from
-// overflow, and normalisation by l makes the result independent of the
-// offset up to rounding.
+// Softmax in base 2.  Every S accumulator starts at -m / (scale*log2(e)),
+// where m is the lane's current offset in base-2 units, so a weight costs one
+// multiply and one exp2.  The offset is not the exact running max: it is
+// raised only when the weights it gives grow too large, which the row sums
+// (bf16-rounded weights added with v_dot2_f32_bf16) reveal without a max
+// reduction.  Then, and on a lane's first valid key, the exact max is taken,
+// O and l are rescaled and the tile's weights are recomputed (a weight that
+// overflowed to inf against a stale offset shows up in the sum as well).
+// Weights stay below 2^12 before normalisation, far from overflow, and the
+// normalisation by l makes the result independent of the offset up to
+// rounding.
 #include "attn_common.h"
 
 #include <type_traits>
@@ -62,9 +62,10 @@ constexpr uint32_t kTileLds = kT * kD * 2;    // 32 KB per K or V tile buffer
 
 struct PPState {
   f32x16 o[4];       // O^T [4 x 32 dims][32 queries]
-  f32x16 s[2];       // S^T - m of the group's 64 keys of the current tile, base-2 units
+  // c2 = scale * log2(e)
+  f32x16 s[2];       // S^T - m/c2 of the group's 64 keys of the current tile (raw score units)
   bf16x8 p[4];       // P^T operands of the previous tile: four 16-key steps
-  f32x16 negm;       // -m broadcast (0 while m is -inf): initial value of S accumulators
+  f32x16 negm;       // -m/c2 broadcast (0 while m is -inf): initial value of S accumulators
   float m;           // offset (base-2 units), -inf until the lane's first valid key
   float l;           // this lane's share of the row sum; the partner lane holds the rest
 };
@@ -122,7 +123,7 @@ struct CopyJob {
 // lane's sum of the bf16-rounded weights.  The copies of `cj` are spread
 // through the work when `copies` is set.
 template <bool SHIFT>
-__device__ __forceinline__ float pp_weights(PPState& st, float sh, const CopyJob& cj, const uint32_t (&dma)[8],
+__device__ __forceinline__ float pp_weights(PPState& st, float c2, float sh, const CopyJob& cj, const uint32_t (&dma)[8],
                                             bool copies) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float rs = 0.f;
@@ -136,7 +137,7 @@ __device__ __forceinline__ float pp_weights(PPState& st, float sh, const CopyJob
     bf16x2 pr[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      float x0 = st.s[kb][8 * hh + 2 * e], x1 = st.s[kb][8 * hh + 2 * e + 1];
+      float x0 = st.s[kb][8 * hh + 2 * e] * c2, x1 = st.s[kb][8 * hh + 2 * e + 1] * c2;
       if constexpr (SHIFT) {
         x0 -= sh;
         x1 -= sh;
@@ -153,7 +154,7 @@ __device__ __forceinline__ float pp_weights(PPState& st, float sh, const CopyJob
 
 // VALU phase: weights of the group's 64 keys of the current tile; `valid` is
 // the number of valid keys among them (0..64).
-__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, const CopyJob& cj,
+__device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float c2, const CopyJob& cj,
                                            const uint32_t (&dma)[8]) {
   if (valid < 64) {
     // key kb*32 + 8*(e>>2) + 4*hl + (e&3) is padding when it is >= valid
@@ -164,15 +165,15 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, const
       for (int e = 0; e < 16; ++e)
         if (kb * 32 + 8 * (e >> 2) + (e & 3) >= vl) st.s[kb][e] = -INFINITY;
   }
-  float rs = pp_weights<false>(st, 0.f, cj, dma, true);
+  float rs = pp_weights<false>(st, c2, 0.f, cj, dma, true);
   // wave-uniform: some lane has no offset yet, or its weights grew too large
   if (__ballot(!(st.m > -INFINITY) || rs > kSumBound) != 0) {
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st.s[kb][e]);
-    mx = pair_max(mx);   // max of s - m over the query's valid keys of this tile
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st.s[kb][e] * c2);
+    mx = pair_max(mx);   // max of c2 * s - m over the query's valid keys of this tile
     float sh;
     if (st.m > -INFINITY) {
       sh = fmaxf(mx, 0.f);
@@ -186,10 +187,10 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, const
       sh = (mx > -INFINITY) ? mx : 0.f;
       st.m = mx;
     }
-    const float nm = (st.m > -INFINITY) ? -st.m : 0.f;
+    const float nm = (st.m > -INFINITY) ? -st.m / c2 : 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) st.negm[e] = nm;
-    rs = pp_weights<true>(st, sh, cj, dma, false);
+    rs = pp_weights<true>(st, c2, sh, cj, dma, false);
   }
   st.l += rs;
 }
@@ -222,8 +223,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
       uint4 u = make_uint4(0, 0, 0, 0);
       if (qvalid) u = *reinterpret_cast<const uint4*>(qp + 16 * ks);
       const bf16x8 raw = as_bf16x8(u);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[ks][e] = (__bf16)(float(raw[e]) * a.scale_log2);
+      qf[ks] = raw;
     }
   }
   // Q is in registers before any page copy is issued, so that the only
@@ -251,6 +251,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   const uint8_t* head_pages = a.pool + (size_t(b) * a.H + h) * a.NT * pbytes;
   const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
   const int count = ((const const_i32*)a.counts)[row];
+  const float c2 = a.scale_log2;
   const int N = count;
   const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
 
@@ -344,12 +345,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     if (grp == 0) {
       mfma_phase(I0{}, F{}, T{}, 0);
       sync();
-      pp_softmax(st, group_valid(0), hl, vjob(1), dma);
+      pp_softmax(st, group_valid(0), hl, c2, vjob(1), dma);
       for (int m = 1; m < N; ++m) {
         top(m);
         mfma_phase(I0{}, T{}, T{}, m);
         sync();
-        pp_softmax(st, group_valid(m), hl, vjob(m + 1), dma);
+        pp_softmax(st, group_valid(m), hl, c2, vjob(m + 1), dma);
       }
       top(N);
       mfma_phase(I0{}, T{}, F{}, N);
@@ -360,12 +361,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
       mfma_phase(I1{}, F{}, T{}, 0);
       for (int m = 1; m < N; ++m) {
         top(m);
-        pp_softmax(st, group_valid(m - 1), hl, kjob(m + 1), dma);
+        pp_softmax(st, group_valid(m - 1), hl, c2, kjob(m + 1), dma);
         sync();
         mfma_phase(I1{}, T{}, T{}, m);
       }
       top(N);
-      pp_softmax(st, group_valid(N - 1), hl, none, dma);
+      pp_softmax(st, group_valid(N - 1), hl, c2, none, dma);
       sync();
       mfma_phase(I1{}, T{}, F{}, N);
     }

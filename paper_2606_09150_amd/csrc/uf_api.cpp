@@ -257,7 +257,8 @@ int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists
 int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
                               void* d_o, float* d_lse, void* stream) {
   if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
-  if (!std::isfinite(scale)) return fail(UF_ERR_ARG, "scale must be finite");
+  if (!(std::isfinite(scale) && scale > 0.f && std::isnormal(scale * 1.4426950408889634f)))
+    return fail(UF_ERR_ARG, "scale must be positive, finite and normal");
   if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
   if (kv->dry()) return ok();
   if (d_q == nullptr || d_o == nullptr || d_lists == nullptr) return fail(UF_ERR_ARG, "q, o or lists is null");

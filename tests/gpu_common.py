@@ -18,7 +18,12 @@ import oracle
 import synth
 
 REL_TOL = 1e-2     # max relative error per row on bf16 O
-LSE_TOL = 2e-3     # absolute error on the fp32 log-sum-exp
+# Absolute error on the fp32 log-sum-exp.  The kernel's row sum l adds the
+# bf16-rounded weights (the same values that multiply V), each within a
+# relative 2^-8 of the exact weight, so ln(l) may differ from the exact value
+# by up to ln(1 + 2^-8) = 3.9e-3 when one key dominates the row; the rest of
+# the bar covers fp32 exponent and accumulation rounding.
+LSE_TOL = 5e-3
 
 
 def require_gpu():
@@ -49,7 +54,7 @@ class Case:
     """One window driven identically on the GPU and in the oracle."""
 
     def __init__(self, P, B, L, H, T, max_chunks, pin_sink, seed, flags=0, gen_device="cpu",
-                 oracle_heads=None):
+                 oracle_heads=None, gain=None):
         self.P = P
         self.B, self.L, self.H, self.T = B, L, H, T
         self.seed = seed
@@ -57,10 +62,13 @@ class Case:
         self.ring = oracle.RingModel(max_chunks, pin_sink)
         self.gen_device = gen_device
         self.oracle_heads = oracle_heads   # None: all heads in the oracle
+        self.gain = gain                   # None, or (chunk, name) -> multiplier of the draw
         self.n_appended = 0
 
     def _draw(self, chunk, name):
         t = synth.custom_tensor((self.B, self.L, self.H, 128), self.seed, chunk, name, device=self.gen_device)
+        if self.gain is not None:
+            t = (t.float() * self.gain(chunk, name)).to(torch.bfloat16)
         return t.cuda() if not t.is_cuda else t
 
     def _host(self, t):

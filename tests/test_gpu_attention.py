@@ -2,7 +2,7 @@
 CPU oracle on the same seeded inputs.
 
 Bar: per (b, h, row) max_d|O_gpu - O_ref| / max_d|O_ref| <= 1e-2 on the bf16
-output, |LSE_gpu - LSE_ref| <= 2e-3.  Full comparison at sizes the oracle
+output, |LSE_gpu - LSE_ref| <= 5e-3.  Full comparison at sizes the oracle
 finishes in seconds (several tiles, ragged tails, T = 64 and 128, batch 2);
 sampled rows at the full workload sizes, in the launch configuration that
 bench.py times; the streaming workload on a fixed head subset.
@@ -59,6 +59,36 @@ def test_small_full_parity(B, L, H, T, mc, pin, n, p):
     for _ in range(n):
         case.append()
     rule = case.rule(p)
+    case.gpu_lists(rule)
+    _full_check(case, rule, case.query())
+
+
+# Score magnitudes far from N(0,1) data: K of chunk c (logical order = append
+# order) multiplied by a per-chunk gain, Q by q_gain.  Rising gains make the
+# row maximum grow from tile to tile by more than the exponent range of fp32
+# (weights against a stale offset overflow to inf and must be recomputed);
+# falling gains make later tiles underflow against the first tile's maximum.
+LOGIT_CASES = [
+    # name, q_gain, k_gain(c)
+    ("rising", 4.0, lambda c: 1.0 + 2.0 * c),
+    ("falling", 4.0, lambda c: 9.0 - 2.0 * c),
+    ("huge", 16.0, lambda c: 4.0 + 4.0 * (c % 2)),
+    ("tiny", 0.01, lambda c: 0.5),
+]
+
+
+@pytest.mark.parametrize("name,q_gain,k_gain", LOGIT_CASES, ids=[c[0] for c in LOGIT_CASES])
+def test_large_and_shifting_logits(name, q_gain, k_gain):
+    P = require_gpu()
+    log(f"attn logits case={name}")
+
+    def gain(chunk, tensor):
+        return q_gain if tensor == "q" else (k_gain(chunk) if tensor == "k" else 1.0)
+
+    case = Case(P, 1, 700, 2, 128, 5, True, seed=4242, gain=gain)
+    for _ in range(5):
+        case.append()
+    rule = case.rule(0.6)
     case.gpu_lists(rule)
     _full_check(case, rule, case.query())
 

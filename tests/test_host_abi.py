@@ -163,7 +163,8 @@ def test_error_paths(P):
         assert status(L.uf_build_tile_lists, w.handle, L.uf_keep_rule(1, p, 1, 1), None, 0) == L.UF_ERR_ARG
     assert status(L.uf_build_tile_lists, w.handle, L.uf_keep_rule(1, 0.5, 2, 1), None, 0) == L.UF_ERR_ARG
     L.uf_build_tile_lists(w.handle, L.uf_keep_rule(1, 0.5, 1, 1), None, 0)
-    assert status(L.uf_sparse_causal_attn_fwd, w.handle, None, None, float("inf"), None) == L.UF_ERR_ARG
+    for bad in (float("inf"), float("nan"), 0.0, -0.1, 1e-45):
+        assert status(L.uf_sparse_causal_attn_fwd, w.handle, None, None, bad, None) == L.UF_ERR_ARG
     L.uf_sparse_causal_attn_fwd(w.handle, None, None, 0.1, None)
     w.append(None, None)
     assert status(L.uf_kv_append, w.handle, None, None) == L.UF_ERR_CAPACITY
