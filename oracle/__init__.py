@@ -18,6 +18,10 @@ It is a plain, slow, obviously correct restatement of what the method computes
                    the paper: their parity against the paper is unpinned; they
                    are pinned to the published SplitMix64 outputs and to
                    binomial statistics.
+* ``topk``      -- the content-adaptive top-k keep set of Eq. 4: mean-pooled
+                   query and key tiles, block scores, top-k per (head, query
+                   tile) with forced pinned/current chunks; fixed float32
+                   arithmetic (parity against the paper unpinned).
 * ``attention`` -- softmax attention of the current chunk's queries over the
                    union of kept key tiles (Eq. 4 mask semantics), computed as
                    masked dense attention in float64.
@@ -35,6 +39,16 @@ from .keep import (
     keep_bits,
     lists_from_bits,
 )
+from .topk import (
+    TopkRule,
+    topk_budget,
+    pooled_means,
+    block_scores,
+    order_key,
+    select_topk,
+    topk_scores,
+    topk_bits,
+)
 from .attention import (
     sparse_causal_attention,
     sparse_causal_attention_rows,
@@ -51,6 +65,14 @@ __all__ = [
     "tile_geometry",
     "keep_bits",
     "lists_from_bits",
+    "TopkRule",
+    "topk_budget",
+    "pooled_means",
+    "block_scores",
+    "order_key",
+    "select_topk",
+    "topk_scores",
+    "topk_bits",
     "sparse_causal_attention",
     "sparse_causal_attention_rows",
     "dense_keys",
