@@ -15,6 +15,8 @@
  *   uf_kv_evict                 drop the oldest non-pinned chunks (host metadata)
  *   uf_kv_append                copy the current chunk's K and V into a free slot
  *   uf_build_tile_lists         per (b, h, query tile) keep lists of key tiles
+ *                               (seeded Bernoulli stand-in), or
+ *   uf_build_topk_lists         the same lists by content-adaptive top-k (Eq. 4)
  *   uf_sparse_causal_attn_fwd   attention of the current chunk's queries
  *
  * Conventions
@@ -92,6 +94,28 @@ typedef struct {
   int32_t keep_current; /* 0 or 1 */
 } uf_keep_rule;
 
+/* Content-adaptive top-k rule for uf_build_topk_lists (Sec. 2.3.1 (b), Eq. 4).
+ * For query tile i of head (b, h) every key tile j of the window gets the score
+ *   s(i, j) = qm(i) . km(j)
+ * where qm(i) is the mean of the valid query tokens of tile i and km(j) the
+ * mean of the valid key tokens of tile j (the block-mean pooling of Eq. 4; the
+ * softmax and the factor 1/sqrt(d) of Eq. 4 are monotone and leave the ranking
+ * unchanged).  Tiles of the pinned chunk (keep_sink) and of the current chunk
+ * (keep_current) are kept without ranking; of the other tiles the `budget`
+ * with the highest scores are kept, equal scores going to the lower logical
+ * index.  Arithmetic is IEEE float32 in a fixed order: a mean is the
+ * sequential sum over tokens in token order divided once by the valid count;
+ * a score adds the rounded products qm[d]*km[d] in order of d, without fused
+ * multiply-add; scores are compared as the unsigned key (bits of s with all
+ * bits flipped when the sign is set, else with the sign bit set), which orders
+ * float32 like the real line.  uf_topk_budget gives Eq. 10's budget. */
+typedef struct {
+  int32_t budget;       /* k >= 0: ranked tiles kept per row (all if k >= candidates) */
+  int32_t keep_sink;    /* 0 or 1 */
+  int32_t keep_current; /* 0 or 1 */
+  int32_t reserved;     /* must be 0 */
+} uf_topk_rule;
+
 typedef struct {
   int32_t n_live;     /* chunks in the window */
   int32_t nq_tiles;   /* NT = ceil(L / T): query tiles = key tiles per chunk */
@@ -121,13 +145,17 @@ typedef struct {
   int32_t reserved;
 } uf_lists_layout;
 
-/* Pool bytes the window needs: max_chunks * B * H * NT pages of 4*T*D bytes.
+/* Pool bytes the window needs: max_chunks * B * H * NT pages of 4*T*D bytes,
+ * then as many pooled keys of D float32 each (4*D bytes).
  * Page of (slot s, b, h, tile t) starts at ((((s*B + b)*H + h)*NT + t) * 4*T*D);
  * it holds K as T rows of D bf16 (row r = token t*T + r of the chunk), then V
  * transposed as D rows of T bf16 in which the keys of each group of 16 are
  * stored with bits 2 and 3 of the key index swapped (column p holds key
  * (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1)).  Rows past the chunk end are 0
- * (9984.0 under UF_F_POISON_PAD).  Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED. */
+ * (9984.0 under UF_F_POISON_PAD).  The pooled key of the same page, the float32
+ * mean of its valid K rows (the key pooling of Eq. 4, written by append), starts
+ * at max_chunks*B*H*NT*4*T*D + ((((s*B + b)*H + h)*NT + t) * 4*D).
+ * Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED. */
 int uf_kv_pool_bytes(const uf_kv_desc* desc, size_t* bytes);
 
 /* Create a handle over a caller-owned pool (256-byte aligned, >= pool bytes).
@@ -168,6 +196,20 @@ int uf_tile_lists_bytes(const uf_kv* kv, size_t* bytes);
  * evict.  Errors: UF_ERR_ARG, UF_ERR_EMPTY (no chunk), UF_ERR_HIP. */
 int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists,
                         size_t bytes, void* stream);
+
+/* Build the keep lists of the current window under the top-k `rule` from the
+ * current chunk's queries d_q [B, L, H, D] bf16 (16-byte aligned) into d_lists
+ * (same layout and validity as uf_build_tile_lists).  The ranked candidates of
+ * a row must number at most 16384.  Errors: UF_ERR_ARG, UF_ERR_EMPTY (no
+ * chunk), UF_ERR_UNSUPPORTED (too many candidates), UF_ERR_HIP. */
+int uf_build_topk_lists(const uf_kv* kv, const void* d_q, const uf_topk_rule* rule,
+                        void* d_lists, size_t bytes, void* stream);
+
+/* Eq. 10's budget: max(k_min, floor(rho * seq_len / seq_ref * n_blocks)) in
+ * double, clamped to int32.  Errors: UF_ERR_ARG (null out, rho < 0 or not
+ * finite, seq_ref < 1, negative counts). */
+int uf_topk_budget(double rho, int64_t seq_len, int64_t seq_ref, int64_t n_blocks, int32_t k_min,
+                   int32_t* budget);
 
 /* Block-sparse chunk-causal attention forward (Eq. 4 mask semantics): for each
  * (b, h) and query row r of the current chunk in query tile i,

@@ -39,6 +39,11 @@ class uf_keep_rule(ctypes.Structure):
                 ("keep_sink", ctypes.c_int32), ("keep_current", ctypes.c_int32)]
 
 
+class uf_topk_rule(ctypes.Structure):
+    _fields_ = [("budget", ctypes.c_int32), ("keep_sink", ctypes.c_int32),
+                ("keep_current", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class uf_kv_info(ctypes.Structure):
     _fields_ = [("n_live", ctypes.c_int32), ("nq_tiles", ctypes.c_int32), ("nk_tiles", ctypes.c_int32),
                 ("tail_valid", ctypes.c_int32), ("first_seq", ctypes.c_int64), ("last_seq", ctypes.c_int64),
@@ -65,6 +70,9 @@ _SIGNATURES = {
     "uf_tile_lists_layout": (ctypes.c_int, [_P, ctypes.POINTER(uf_lists_layout)]),
     "uf_tile_lists_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "uf_build_tile_lists": (ctypes.c_int, [_P, ctypes.POINTER(uf_keep_rule), _P, ctypes.c_size_t, _P]),
+    "uf_build_topk_lists": (ctypes.c_int, [_P, _P, ctypes.POINTER(uf_topk_rule), _P, ctypes.c_size_t, _P]),
+    "uf_topk_budget": (ctypes.c_int, [ctypes.c_double, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                      ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
     "uf_sparse_causal_attn_fwd": (ctypes.c_int, [_P, _P, _P, ctypes.c_float, _P, _P, _P]),
     "uf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "uf_last_error": (ctypes.c_char_p, []),
@@ -175,6 +183,18 @@ def uf_build_tile_lists(handle, rule: uf_keep_rule, lists, nbytes: int = None, s
     n = nbytes if nbytes is not None else (0 if lists is None else lists.numel() * lists.element_size())
     s = None if lists is None else _stream_ptr(stream)
     _check(load().uf_build_tile_lists(handle, ctypes.byref(rule), _ptr(lists), n, s))
+
+
+def uf_build_topk_lists(handle, q, rule: uf_topk_rule, lists, nbytes: int = None, stream=None) -> None:
+    n = nbytes if nbytes is not None else (0 if lists is None else lists.numel() * lists.element_size())
+    s = None if lists is None else _stream_ptr(stream)
+    _check(load().uf_build_topk_lists(handle, _ptr(q), ctypes.byref(rule), _ptr(lists), n, s))
+
+
+def uf_topk_budget(rho: float, seq_len: int, seq_ref: int, n_blocks: int, k_min: int = 4) -> int:
+    out = ctypes.c_int32(0)
+    _check(load().uf_topk_budget(ctypes.c_double(rho), seq_len, seq_ref, n_blocks, k_min, ctypes.byref(out)))
+    return out.value
 
 
 def uf_sparse_causal_attn_fwd(handle, q, lists, scale: float, o, lse=None, stream=None) -> None:

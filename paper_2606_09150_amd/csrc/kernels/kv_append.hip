@@ -7,7 +7,11 @@
 // stores); V is staged in LDS and written transposed ([D][T]) with the keys of
 // every group of 16 stored in swap23 order, which is the order in which the
 // attention kernel's 32x32x16 MFMA consumes them.  Rows past the chunk end get
-// the pad value.  HBM-bound: 2*B*L*H*D*2 bytes read, 2*B*NT*T*H*D*2 written.
+// the pad value.  The page's pooled key (the block-mean pooling of Eq. 4,
+// Sec. 2.3.1 (b)) is written beside it: the float32 mean of the valid K rows,
+// summed in token order and divided once by their count, so that the top-k
+// list builder ranks tiles with a fixed arithmetic.  HBM-bound: 2*B*L*H*D*2
+// bytes read, 2*B*NT*T*H*D*2 + B*NT*H*D*4 written.
 #include "../launch.h"
 
 namespace uf {
@@ -62,6 +66,23 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a) {
       w[e] = lo | (hi << 16);
     }
     vdst[c] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+
+  // Pooled key: the valid K rows are staged again (L2-resident since the
+  // copy above read them) in the V stage, then lane d adds column d in order.
+  __syncthreads();
+  for (int c = threadIdx.x; c < valid * kRowChunks; c += kThreads) {
+    const int r = c / kRowChunks;
+    const int cc = c % kRowChunks;
+    const size_t off = ((size_t(b) * a.L + size_t(t) * T + r) * a.H + h) * kD + cc * 8;
+    vstage[r * kStage + cc] = *reinterpret_cast<const uint4*>(a.k + off);
+  }
+  __syncthreads();
+  if (threadIdx.x < kD) {
+    const int d = threadIdx.x;
+    float acc = 0.f;
+    for (int r = 0; r < valid; ++r) acc += __uint_as_float(uint32_t(vs[r * (kStage * 8) + d]) << 16);
+    a.kmean[(size_t(a.slot) * a.B * a.H * a.NT + size_t(page)) * kD + d] = acc / float(valid);
   }
 }
 

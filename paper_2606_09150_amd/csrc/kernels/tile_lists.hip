@@ -7,17 +7,15 @@
 // key tile kept iff the upper 32 bits of a SplitMix64 chain over
 // (b, h, seq(current), i, seq(chunk), t) fall below floor(p * 2^32).
 //
-// One workgroup of 256 lanes per list row; each pass decides 256 consecutive
-// logical tiles, a wave ballot gives two 32-bit mask words per wave, and a
-// prefix over the four wave counts places the kept indices in ascending order.
-// Integer-only, so the lists are bit-exact.
-#include "../launch.h"
+// One workgroup of 256 lanes per list row; the row is written by the shared
+// output stage (list_emit.h).  Integer-only, so the lists are bit-exact.
+#include "list_emit.h"
 
 namespace uf {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
+using lists::kThreads;
+using lists::kWaves;
 
 // One SplitMix64 step (Steele, Lea, Flood, OOPSLA 2014): golden-ratio
 // increment, then the 64-bit finaliser.
@@ -36,9 +34,6 @@ __global__ __launch_bounds__(kThreads) void tile_lists_kernel(ListArgs a) {
   const int bh = row / a.NT;
   const int h = bh % a.H;
   const int b = bh / a.H;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-
   uint64_t x = a.seed;
   x = splitmix64(x ^ uint64_t(b));
   x = splitmix64(x ^ uint64_t(h));
@@ -49,40 +44,16 @@ __global__ __launch_bounds__(kThreads) void tile_lists_kernel(ListArgs a) {
   int32_t* idx = reinterpret_cast<int32_t*>(a.lists + a.idx_offset) + size_t(row) * a.nk_cap;
   uint32_t* mask = reinterpret_cast<uint32_t*>(a.lists + a.mask_offset) + size_t(row) * a.mask_words;
 
-  int base = 0;
-  for (int j0 = 0; j0 < a.nk_cap; j0 += kThreads) {
-    const int j = j0 + threadIdx.x;
-    bool keep = false;
-    if (j < a.nk) {
-      const int pos = j / a.NT;
-      const int t = j - pos * a.NT;
-      const bool forced = (a.sink[pos] && a.keep_sink) || (a.seq[pos] == a.cur_seq && a.keep_current);
-      if (forced) {
-        keep = true;
-      } else {
-        uint64_t y = splitmix64(x ^ uint64_t(a.seq[pos]));
-        y = splitmix64(y ^ uint64_t(t));
-        keep = (y >> 32) < a.thr;
-      }
-    }
-    const uint64_t ballot = __ballot(keep);
-    const int w0 = (j0 + wave * 64) >> 5;
-    if (lane == 0 && w0 < a.mask_words) mask[w0] = uint32_t(ballot);
-    if (lane == 0 && w0 + 1 < a.mask_words) mask[w0 + 1] = uint32_t(ballot >> 32);
-    if (lane == 0) wave_count[wave] = __popcll(ballot);
-    __syncthreads();
-    int off = base, total = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      off += (w < wave) ? wave_count[w] : 0;
-      total += wave_count[w];
-    }
-    if (keep) idx[off + __popcll(ballot & ((1ull << lane) - 1ull))] = j;
-    __syncthreads();
-    base += total;
-  }
-  for (int j = base + threadIdx.x; j < a.nk_cap; j += kThreads) idx[j] = -1;
-  if (threadIdx.x == 0) counts[row] = base;
+  auto keep_of = [&](int j) {
+    if (j >= a.nk) return false;
+    const int pos = j / a.NT;
+    const int t = j - pos * a.NT;
+    if ((a.sink[pos] && a.keep_sink) || (a.seq[pos] == a.cur_seq && a.keep_current)) return true;
+    uint64_t y = splitmix64(x ^ uint64_t(a.seq[pos]));
+    y = splitmix64(y ^ uint64_t(t));
+    return (y >> 32) < a.thr;
+  };
+  lists::emit_row(keep_of, a.nk_cap, a.mask_words, counts + row, idx, mask, wave_count);
 }
 
 }  // namespace

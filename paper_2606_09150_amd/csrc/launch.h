@@ -23,6 +23,7 @@ struct AppendArgs {
   const uint16_t* k;      // [B, L, H, D]
   const uint16_t* v;      // [B, L, H, D]
   uint8_t* pool;
+  float* kmean;           // pooled keys of the pool: [slots][B][H][NT][D]
   int64_t slot;
   int32_t B, H, L, T, NT, tail;
   uint16_t pad;           // bf16 bits written into padding rows
@@ -42,6 +43,21 @@ struct ListArgs {
   int32_t sink[UF_MAX_CHUNKS];  // 1 if logical position holds the pinned chunk
 };
 hipError_t launch_tile_lists(const ListArgs& a, hipStream_t stream);
+
+// Top-k lists: one workgroup per (b, h, group of G query tiles).
+struct TopkArgs {
+  const uint16_t* q;      // [B, L, H, D]
+  const float* kmean;     // pooled keys: [slots][B][H][NT][D]
+  uint8_t* lists;
+  size_t idx_offset, mask_offset;
+  int32_t B, H, L, T, NT, tail, nk, nk_cap, mask_words;
+  int32_t G;              // query tiles per workgroup
+  int32_t cand_lo, cand_hi;   // ranked logical tiles [cand_lo, cand_hi)
+  int32_t budget;
+  int32_t slot_of[UF_MAX_CHUNKS];
+};
+constexpr int kTopkMaxCandidates = 16384;   // G * candidates per workgroup
+hipError_t launch_topk_lists(const TopkArgs& a, size_t lds_bytes, hipStream_t stream);
 
 struct AttnArgs {
   const uint16_t* q;      // [B, L, H, D]

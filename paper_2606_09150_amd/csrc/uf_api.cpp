@@ -8,6 +8,8 @@
 // logical order is ascending append sequence number, so an optional pinned
 // first chunk always sits at logical position 0; eviction frees the oldest
 // non-pinned slots and moves no data.
+#include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -68,6 +70,11 @@ int check_desc(const uf_kv_desc* d) {
 struct uf_kv {
   uf_kv_desc d;
   uint8_t* pool;
+  // pooled keys follow the pages: [max_chunks][B][H][NT][D] float32
+  float* kmean() const {
+    const size_t pages = size_t(d.max_chunks) * d.batch * d.heads * nt;
+    return reinterpret_cast<float*>(pool + pages * uf::page_bytes(d.tile, d.head_dim));
+  }
   size_t pool_bytes;
   int32_t nt;
   int32_t tail;
@@ -99,7 +106,8 @@ int uf_kv_pool_bytes(const uf_kv_desc* desc, size_t* bytes) {
   if (int s = check_desc(desc)) return s;
   if (bytes == nullptr) return fail(UF_ERR_ARG, "bytes is null");
   const size_t nt = (size_t(desc->chunk_tokens) + desc->tile - 1) / desc->tile;
-  *bytes = size_t(desc->max_chunks) * desc->batch * desc->heads * nt * uf::page_bytes(desc->tile, desc->head_dim);
+  const size_t pages = size_t(desc->max_chunks) * desc->batch * desc->heads * nt;
+  *bytes = pages * (uf::page_bytes(desc->tile, desc->head_dim) + size_t(4) * desc->head_dim);
   return ok();
 }
 
@@ -145,6 +153,7 @@ int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream) {
     a.k = static_cast<const uint16_t*>(d_k);
     a.v = static_cast<const uint16_t*>(d_v);
     a.pool = kv->pool;
+    a.kmean = kv->kmean();
     a.slot = slot;
     a.B = kv->d.batch;
     a.H = kv->d.heads;
@@ -251,6 +260,63 @@ int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists
   }
   hipError_t e = uf::launch_tile_lists(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "tile_lists launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_build_topk_lists(const uf_kv* kv, const void* d_q, const uf_topk_rule* rule, void* d_lists,
+                        size_t bytes, void* stream) {
+  if (kv == nullptr || rule == nullptr) return fail(UF_ERR_ARG, "null argument");
+  if (rule->budget < 0) return fail(UF_ERR_ARG, "budget must be >= 0 (got %d)", rule->budget);
+  if ((rule->keep_sink != 0 && rule->keep_sink != 1) || (rule->keep_current != 0 && rule->keep_current != 1))
+    return fail(UF_ERR_ARG, "keep_sink and keep_current must be 0 or 1");
+  if (rule->reserved != 0) return fail(UF_ERR_ARG, "reserved must be 0");
+  if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
+  const int32_t nk = int32_t(kv->live.size()) * kv->nt;
+  const int32_t lo = (kv->live.front().sink && rule->keep_sink) ? kv->nt : 0;
+  const int32_t hi = rule->keep_current ? nk - kv->nt : nk;
+  const int32_t nc = std::max(hi - lo, 0);
+  if (nc > uf::kTopkMaxCandidates)
+    return fail(UF_ERR_UNSUPPORTED, "%d ranked candidates per row, at most %d", nc, uf::kTopkMaxCandidates);
+  const uf_lists_layout lay = kv->layout();
+  if (kv->dry()) return ok();
+  if (d_q == nullptr || !aligned(d_q, 16)) return fail(UF_ERR_ARG, "q must be non-null and 16-byte aligned");
+  if (d_lists == nullptr || !aligned(d_lists, 256)) return fail(UF_ERR_ARG, "lists must be non-null and 256-byte aligned");
+  if (bytes < lay.total_bytes) return fail(UF_ERR_ARG, "lists buffer has %zu bytes, needs %zu", bytes, lay.total_bytes);
+  uf::TopkArgs a{};
+  a.q = static_cast<const uint16_t*>(d_q);
+  a.kmean = kv->kmean();
+  a.lists = static_cast<uint8_t*>(d_lists);
+  a.idx_offset = lay.idx_offset;
+  a.mask_offset = lay.mask_offset;
+  a.B = kv->d.batch;
+  a.H = kv->d.heads;
+  a.L = kv->d.chunk_tokens;
+  a.T = kv->d.tile;
+  a.NT = kv->nt;
+  a.tail = kv->tail;
+  a.nk = nk;
+  a.nk_cap = kv->nk_cap;
+  a.mask_words = kv->mask_words;
+  a.G = std::max(1, std::min({8, kv->nt, uf::kTopkMaxCandidates / std::max(nc, 1)}));
+  a.cand_lo = lo;
+  a.cand_hi = hi;
+  a.budget = rule->budget;
+  for (size_t p = 0; p < kv->live.size(); ++p) a.slot_of[p] = kv->live[p].slot;
+  const size_t lds = std::max<size_t>(size_t(a.G) * size_t(nc) * 5, 16);
+  hipError_t e = uf::launch_topk_lists(a, lds, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "topk_lists launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_topk_budget(double rho, int64_t seq_len, int64_t seq_ref, int64_t n_blocks, int32_t k_min,
+                   int32_t* budget) {
+  if (budget == nullptr) return fail(UF_ERR_ARG, "budget is null");
+  if (!(std::isfinite(rho) && rho >= 0.0)) return fail(UF_ERR_ARG, "rho must be finite and >= 0");
+  if (seq_ref < 1 || seq_len < 0 || n_blocks < 0 || k_min < 0)
+    return fail(UF_ERR_ARG, "seq_ref must be >= 1 and the counts >= 0");
+  const double k = std::floor(rho * double(seq_len) / double(seq_ref) * double(n_blocks));
+  const double c = std::min(std::max(k, double(k_min)), double(INT32_MAX));
+  *budget = int32_t(c);
   return ok();
 }
 

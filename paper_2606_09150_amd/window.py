@@ -80,6 +80,22 @@ class KVWindow:
         L.uf_build_tile_lists(self.handle, rule, self.lists, None, stream)
         return self.lists
 
+    def build_topk_lists(self, q, budget, keep_sink=True, keep_current=True, stream=None):
+        """Lists by content-adaptive top-k from the current chunk's queries q [B, L, H, D] bf16."""
+        if not self.dry:
+            _check_chunk(q, "q", self.B, self.L, self.H, self.D)
+        rule = L.uf_topk_rule(int(budget), int(keep_sink), int(keep_current), 0)
+        L.uf_build_topk_lists(self.handle, q, rule, self.lists, None, stream)
+        return self.lists
+
+    def kmean_view(self):
+        """Pooled keys [max_chunks, B, H, NT, D] float32 (the pool's tail section)."""
+        nt = -(-self.L // self.T)
+        pages = self.desc.max_chunks * self.B * self.H * nt
+        off = pages * 4 * self.T * self.D
+        return self.pool[off:off + pages * self.D * 4].view(torch.float32).view(
+            self.desc.max_chunks, self.B, self.H, nt, self.D)
+
     def lists_views(self, lists=None):
         """(counts [B,H,NT], idx [B,H,NT,nk_cap], mask [B,H,NT,words]) views of a list buffer."""
         buf = self.lists if lists is None else lists

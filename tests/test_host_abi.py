@@ -34,7 +34,7 @@ def _declared():
 def test_library_exports_every_declared_symbol(P):
     from paper_2606_09150_amd import _lib
     names = _declared()
-    assert len(names) == 13
+    assert len(names) == 15
     lib = ctypes.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -105,7 +105,7 @@ def test_geometry_and_layout(P):
     assert lay.idx_offset >= 4 * rows
     assert lay.mask_offset >= lay.idx_offset + 4 * rows * 960
     assert lay.total_bytes >= lay.mask_offset + 4 * rows * 30
-    assert w.pool_bytes == 5 * 12 * 192 * 4 * 128 * 128
+    assert w.pool_bytes == 5 * 12 * 192 * (4 * 128 * 128 + 4 * 128)   # pages, then pooled keys
 
 
 def test_error_paths(P):
@@ -177,3 +177,37 @@ def test_error_paths(P):
         assert L.uf_status_string(code).startswith("UF_ERR_")
     assert status(L.uf_kv_evict, None, 1) == L.UF_ERR_ARG
     assert "null" in L.uf_last_error()
+
+
+def test_topk_host_paths(P):
+    """Top-k builder checks that need no device, and Eq. 10's budget helper."""
+    L = P._lib
+    E = P.UfError
+
+    def status(fn, *a):
+        with pytest.raises(E) as ei:
+            fn(*a)
+        return ei.value.status
+
+    w = _dry(P, max_chunks=4, L=300, T=128)
+    assert status(L.uf_build_topk_lists, w.handle, None, L.uf_topk_rule(3, 1, 1, 0), None, 0) == L.UF_ERR_EMPTY
+    w.append(None, None)
+    w.append(None, None)
+    L.uf_build_topk_lists(w.handle, None, L.uf_topk_rule(3, 1, 1, 0), None, 0)      # dry run: no device work
+    for rule in (L.uf_topk_rule(-1, 1, 1, 0), L.uf_topk_rule(1, 2, 1, 0), L.uf_topk_rule(1, 1, -1, 0),
+                 L.uf_topk_rule(1, 1, 1, 7)):
+        assert status(L.uf_build_topk_lists, w.handle, None, rule, None, 0) == L.UF_ERR_ARG
+    # more ranked candidates per row than the builder supports
+    big = _dry(P, max_chunks=4, L=128 * 8200, T=128, H=1)
+    for _ in range(3):
+        big.append(None, None)
+    assert status(L.uf_build_topk_lists, big.handle, None, L.uf_topk_rule(5, 0, 0, 0), None, 0) == L.UF_ERR_UNSUPPORTED
+    L.uf_build_topk_lists(big.handle, None, L.uf_topk_rule(5, 1, 1, 0), None, 0)     # 8200 candidates: fine
+    # Eq. 10 through the C helper agrees with the oracle's helper
+    for rho, S, Sr, n, kmin in ((1.0, 1560, 1560, 200, 4), (1.0, 8160, 1560, 960, 4), (0.25, 1560, 1560, 576, 4),
+                                (0.7, 100, 1560, 10, 4), (2.0, 14400, 1560, 1352, 0), (0.0, 5, 7, 9, 3)):
+        assert L.uf_topk_budget(rho, S, Sr, n, kmin) == oracle.topk_budget(rho, S, Sr, n, kmin)
+    assert L.uf_topk_budget(1e9, 10 ** 9, 1, 10 ** 9, 0) == 2 ** 31 - 1                 # clamped
+    for args in ((-1.0, 1, 1, 1, 0), (float("nan"), 1, 1, 1, 0), (1.0, 1, 0, 1, 0), (1.0, -1, 1, 1, 0),
+                 (1.0, 1, 1, 1, -1)):
+        assert status(L.uf_topk_budget, *args) == L.UF_ERR_ARG
