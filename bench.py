@@ -141,7 +141,7 @@ def run_workload(P, wl, steps, warmup, n_src=3):
     dense = 4 * D * B * H * L * (L * wl.window_chunks)
     attn_avg = sum(attn_ms) / steps
     attn_sorted = sorted(attn_ms)
-    append_bytes = 2 * B * L * H * D * 2 + 2 * B * nt * T * H * D * 2
+    append_bytes = 2 * B * L * H * D * 2 + 2 * B * nt * T * H * D * 2 + B * nt * H * D * 4
     res = {
         "workload": wl.name,
         "ms_per_step": ms_step,
@@ -158,6 +158,21 @@ def run_workload(P, wl, steps, warmup, n_src=3):
         "padded_tile_tflop_per_step": padded / 1e12,
         "keys": L * wl.window_chunks,
     }
+    # content-adaptive top-k lists (Eq. 4) on the final window, with the budget
+    # that keeps the same expected number of earlier-chunk tiles as p_prior
+    budget = int(wl.p_prior * wl.prior_chunks * nt)
+    q_cur = srcs[(wl.window_chunks - 1 + total - 1) % n_src]["q"]
+    tk = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    win.lists = lists[0]
+    for _ in range(2):
+        win.build_topk_lists(q_cur, budget)
+    tk[0].record(stream)
+    for _ in range(10):
+        win.build_topk_lists(q_cur, budget)
+    tk[1].record(stream)
+    torch.cuda.synchronize()
+    res["topk_budget"] = budget
+    res["topk_lists_us"] = tk[0].elapsed_time(tk[1]) / 10 * 1e3
     state = {"win": win, "srcs": srcs, "n_src": n_src, "steps_done": total}
     return res, state
 
@@ -274,7 +289,7 @@ def main():
                    "pinned_first_chunk": wl.pin_sink},
     }
     for k in ("attn_ms", "attn_ms_p10", "attn_ms_p90", "attn_tflops", "append_us", "append_gbps", "lists_us",
-              "kept_tflop_per_step", "kept_fraction", "padded_tile_tflop_per_step"):
+              "topk_budget", "topk_lists_us", "kept_tflop_per_step", "kept_fraction", "padded_tile_tflop_per_step"):
         line[k] = res[k]
     line["roofline"] = {
         "bound": "mfma",

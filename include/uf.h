@@ -132,12 +132,15 @@ typedef struct {
  *   counts  int32 [R]               kept key tiles of the row
  *   idx     int32 [R][nk_cap]       kept logical key tiles, ascending, then -1
  *   mask    uint32[R][mask_words]   bit j%32 of word j/32 set iff tile j kept
+ *   scratch float [R][D]            working memory of uf_build_topk_lists (the
+ *                                   pooled queries); contents unspecified
  * Logical key tile j is tile j % NT of the chunk at logical position j / NT;
  * logical order is [pinned chunk][oldest earlier .. newest earlier][current]. */
 typedef struct {
   size_t counts_offset;
   size_t idx_offset;
   size_t mask_offset;
+  size_t scratch_offset;
   size_t total_bytes;
   int32_t rows;
   int32_t nk_cap;

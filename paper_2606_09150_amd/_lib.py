@@ -52,7 +52,8 @@ class uf_kv_info(ctypes.Structure):
 
 class uf_lists_layout(ctypes.Structure):
     _fields_ = [("counts_offset", ctypes.c_size_t), ("idx_offset", ctypes.c_size_t),
-                ("mask_offset", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t),
+                ("mask_offset", ctypes.c_size_t), ("scratch_offset", ctypes.c_size_t),
+                ("total_bytes", ctypes.c_size_t),
                 ("rows", ctypes.c_int32), ("nk_cap", ctypes.c_int32), ("mask_words", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
 

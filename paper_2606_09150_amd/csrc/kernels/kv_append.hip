@@ -81,6 +81,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a) {
   if (threadIdx.x < kD) {
     const int d = threadIdx.x;
     float acc = 0.f;
+#pragma unroll 8
     for (int r = 0; r < valid; ++r) acc += __uint_as_float(uint32_t(vs[r * (kStage * 8) + d]) << 16);
     a.kmean[(size_t(a.slot) * a.B * a.H * a.NT + size_t(page)) * kD + d] = acc / float(valid);
   }

@@ -49,7 +49,7 @@ struct TopkArgs {
   const uint16_t* q;      // [B, L, H, D]
   const float* kmean;     // pooled keys: [slots][B][H][NT][D]
   uint8_t* lists;
-  size_t idx_offset, mask_offset;
+  size_t idx_offset, mask_offset, scratch_offset;   // scratch: pooled queries [B][H][NT][D]
   int32_t B, H, L, T, NT, tail, nk, nk_cap, mask_words;
   int32_t G;              // query tiles per workgroup
   int32_t cand_lo, cand_hi;   // ranked logical tiles [cand_lo, cand_hi)

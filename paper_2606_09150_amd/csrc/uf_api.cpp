@@ -95,7 +95,8 @@ struct uf_kv {
     lay.counts_offset = 0;
     lay.idx_offset = up(size_t(lay.rows) * 4);
     lay.mask_offset = lay.idx_offset + up(size_t(lay.rows) * size_t(nk_cap) * 4);
-    lay.total_bytes = lay.mask_offset + up(size_t(lay.rows) * size_t(mask_words) * 4);
+    lay.scratch_offset = lay.mask_offset + up(size_t(lay.rows) * size_t(mask_words) * 4);
+    lay.total_bytes = lay.scratch_offset + up(size_t(lay.rows) * size_t(d.head_dim) * 4);
     return lay;
   }
 };
@@ -288,6 +289,7 @@ int uf_build_topk_lists(const uf_kv* kv, const void* d_q, const uf_topk_rule* ru
   a.lists = static_cast<uint8_t*>(d_lists);
   a.idx_offset = lay.idx_offset;
   a.mask_offset = lay.mask_offset;
+  a.scratch_offset = lay.scratch_offset;
   a.B = kv->d.batch;
   a.H = kv->d.heads;
   a.L = kv->d.chunk_tokens;
@@ -297,7 +299,7 @@ int uf_build_topk_lists(const uf_kv* kv, const void* d_q, const uf_topk_rule* ru
   a.nk = nk;
   a.nk_cap = kv->nk_cap;
   a.mask_words = kv->mask_words;
-  a.G = std::max(1, std::min({8, kv->nt, uf::kTopkMaxCandidates / std::max(nc, 1)}));
+  a.G = std::max(1, std::min({2, kv->nt, uf::kTopkMaxCandidates / std::max(nc, 1)}));
   a.cand_lo = lo;
   a.cand_hi = hi;
   a.budget = rule->budget;

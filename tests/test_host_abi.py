@@ -104,7 +104,8 @@ def test_geometry_and_layout(P):
     assert lay.counts_offset == 0 and lay.idx_offset % 256 == 0 and lay.mask_offset % 256 == 0
     assert lay.idx_offset >= 4 * rows
     assert lay.mask_offset >= lay.idx_offset + 4 * rows * 960
-    assert lay.total_bytes >= lay.mask_offset + 4 * rows * 30
+    assert lay.scratch_offset % 256 == 0 and lay.scratch_offset >= lay.mask_offset + 4 * rows * 30
+    assert lay.total_bytes >= lay.scratch_offset + 4 * rows * 128
     assert w.pool_bytes == 5 * 12 * 192 * (4 * 128 * 128 + 4 * 128)   # pages, then pooled keys
 
 
