@@ -177,6 +177,42 @@ def run_workload(P, wl, steps, warmup, n_src=3):
     return res, state
 
 
+def sparsity_sweep(wl, state, sparsities=(0.12, 0.35, 0.58, 0.72, 0.82), reps=10):
+    """Attention time against sparsity on the final window of a run (the shape of the
+    paper's sparsity-ratio ablation, App. L): pure top-k lists over the whole window
+    (no forced chunks), budget = (1 - sparsity) * key tiles per row."""
+    import torch
+
+    win = state["win"]
+    srcs, n_src = state["srcs"], state["n_src"]
+    B, L, H, T = wl.batch, wl.chunk_tokens, wl.heads, wl.tile
+    nt = -(-L // T)
+    tail = L - (nt - 1) * T
+    nk = win.info().nk_tiles
+    q = srcs[(wl.window_chunks - 1 + state["steps_done"] - 1) % n_src]["q"]
+    out = torch.empty((B, L, H, D), dtype=torch.bfloat16, device=q.device)
+    lse = torch.empty((B, H, L), dtype=torch.float32, device=q.device)
+    stream = torch.cuda.current_stream()
+    dense = 4 * D * B * H * L * (L * win.info().n_live)
+    rows = []
+    for sp in sparsities:
+        budget = int(round((1.0 - sp) * nk))
+        win.build_topk_lists(q, budget, keep_sink=False, keep_current=False)
+        for _ in range(2):
+            win.attention(q, out=out, lse=lse)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record(stream)
+        for _ in range(reps):
+            win.attention(q, out=out, lse=lse)
+        e[1].record(stream)
+        torch.cuda.synchronize()
+        ms = e[0].elapsed_time(e[1]) / reps
+        kept, _ = _flops_of_lists(win, win.lists, nt, tail, T)
+        rows.append({"target_sparsity": sp, "budget": budget, "sparsity": 1.0 - kept / dense,
+                     "attn_ms": ms, "tflops": kept / (ms * 1e-3) / 1e12})
+    return rows
+
+
 def cpu_baseline(wl, state, target_s):
     """The oracle, as it stands, on a bounded sample: head 0 of the last window, leading q-tiles."""
     import numpy as np
@@ -246,6 +282,8 @@ def main():
     ap.add_argument("--secondary", default="2k", help="second workload reported in the same line ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time the attention against sparsity (top-k lists, no forced chunks)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB three times with a plain device copy "
                          "(reference dispatches for scaling hardware byte counters)")
@@ -299,6 +337,8 @@ def main():
         "frac": res["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS,
         "traffic": measured_traffic(wl.name),
     }
+    if args.sweep:
+        line["sweep"] = sparsity_sweep(wl, state)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, state, args.cpu_seconds)
     del state

@@ -176,6 +176,16 @@ int uf_kv_destroy(uf_kv* kv);
  * sequence number.  Errors: UF_ERR_ARG, UF_ERR_CAPACITY (window full), UF_ERR_HIP. */
 int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream);
 
+/* Refresh the current chunk in place (Sec. 2.3.2 (ii), adaptive cache
+ * refresh: the KV entries of the newest chunk are recomputed and replace the
+ * ones appended from the last denoising step): copy K and V [B, L, H, D] bf16
+ * (16-byte aligned) over the current chunk's pages and pooled keys.  Its
+ * sequence number and logical position do not change, so Bernoulli lists are
+ * unchanged and top-k lists must be rebuilt.  Reads of the old pages already
+ * enqueued on the same stream happen first.  Errors: UF_ERR_ARG, UF_ERR_EMPTY
+ * (no chunk), UF_ERR_HIP. */
+int uf_kv_replace_newest(uf_kv* kv, const void* d_k, const void* d_v, void* stream);
+
 /* Drop the n oldest chunks that are not pinned (Sec. 2.3.2 (iii): a compact
  * cache window).  Host metadata only: the freed slot is rewritten by a later
  * append, which the stream orders after already-enqueued reads on that same

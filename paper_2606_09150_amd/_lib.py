@@ -65,6 +65,7 @@ _SIGNATURES = {
     "uf_kv_destroy": (ctypes.c_int, [_P]),
     "uf_kv_append": (ctypes.c_int, [_P, _P, _P, _P]),
     "uf_kv_evict": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "uf_kv_replace_newest": (ctypes.c_int, [_P, _P, _P, _P]),
     "uf_kv_get_info": (ctypes.c_int, [_P, ctypes.POINTER(uf_kv_info)]),
     "uf_kv_logical": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
                                      ctypes.POINTER(ctypes.c_int64)]),
@@ -150,6 +151,11 @@ def uf_kv_destroy(handle) -> None:
 def uf_kv_append(handle, k, v, stream=None) -> None:
     s = None if (k is None and v is None) else _stream_ptr(stream)
     _check(load().uf_kv_append(handle, _ptr(k), _ptr(v), s))
+
+
+def uf_kv_replace_newest(handle, k, v, stream=None) -> None:
+    s = None if k is None else _stream_ptr(stream)
+    _check(load().uf_kv_replace_newest(handle, _ptr(k), _ptr(v), s))
 
 
 def uf_kv_evict(handle, n_chunks: int) -> None:

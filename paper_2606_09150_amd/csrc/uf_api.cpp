@@ -141,12 +141,10 @@ int uf_kv_destroy(uf_kv* kv) {
   return ok();
 }
 
-int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream) {
-  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
-  if (int32_t(kv->live.size()) >= kv->d.max_chunks)
-    return fail(UF_ERR_CAPACITY, "window full (%d chunks)", kv->d.max_chunks);
-  int32_t slot = 0;
-  while (kv->used[size_t(slot)]) ++slot;
+namespace {
+
+// Copy one chunk's K and V into the pages (and pooled keys) of `slot`.
+int write_chunk(uf_kv* kv, int32_t slot, const void* d_k, const void* d_v, void* stream) {
   if (!kv->dry()) {
     if (d_k == nullptr || d_v == nullptr) return fail(UF_ERR_ARG, "k or v is null");
     if (!aligned(d_k, 16) || !aligned(d_v, 16)) return fail(UF_ERR_ARG, "k and v must be 16-byte aligned");
@@ -166,9 +164,28 @@ int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream) {
     hipError_t e = uf::launch_kv_append(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(UF_ERR_HIP, "kv_append launch: %s", hipGetErrorString(e));
   }
+  return UF_OK;
+}
+
+}  // namespace
+
+int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (int32_t(kv->live.size()) >= kv->d.max_chunks)
+    return fail(UF_ERR_CAPACITY, "window full (%d chunks)", kv->d.max_chunks);
+  int32_t slot = 0;
+  while (kv->used[size_t(slot)]) ++slot;
+  if (int s = write_chunk(kv, slot, d_k, d_v, stream)) return s;
   const int64_t seq = kv->next_seq++;
   kv->used[size_t(slot)] = 1;
   kv->live.push_back(Live{slot, seq, kv->d.pin_sink == 1 && seq == 0});
+  return ok();
+}
+
+int uf_kv_replace_newest(uf_kv* kv, const void* d_k, const void* d_v, void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
+  if (int s = write_chunk(kv, kv->live.back().slot, d_k, d_v, stream)) return s;
   return ok();
 }
 

@@ -65,6 +65,13 @@ class KVWindow:
             _check_chunk(v, "v", self.B, self.L, self.H, self.D)
         L.uf_kv_append(self.handle, k, v, stream)
 
+    def replace_newest(self, k, v, stream=None):
+        """Refresh the current chunk's K and V in place (same sequence number)."""
+        if not self.dry:
+            _check_chunk(k, "k", self.B, self.L, self.H, self.D)
+            _check_chunk(v, "v", self.B, self.L, self.H, self.D)
+        L.uf_kv_replace_newest(self.handle, k, v, stream)
+
     def evict(self, n=1):
         L.uf_kv_evict(self.handle, n)
 

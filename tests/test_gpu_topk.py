@@ -145,3 +145,31 @@ def test_attention_over_topk_lists():
     lerr = float(np.abs(f64(lse) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL and lerr <= LSE_TOL
+
+
+def test_replace_newest_equals_appending_the_refreshed_chunk():
+    """A refreshed current chunk (Sec. 2.3.2 (ii)) gives the same pages, pooled keys,
+    lists and attention as a window that appended the refreshed K/V directly."""
+    P = require_gpu()
+    shape = (1, 300, 2, 128)
+    kv = [(synth.custom_tensor(shape, 8, c, "k").cuda(), synth.custom_tensor(shape, 8, c, "v").cuda())
+          for c in range(5)]
+    q = synth.custom_tensor(shape, 8, 9, "q").cuda()
+    wa = P.KVWindow(1, 2, 300, 128, 4, True)
+    wb = P.KVWindow(1, 2, 300, 128, 4, True)
+    for c in range(4):
+        wa.append(*kv[c])
+    wa.replace_newest(*kv[4])                   # chunk 3 refreshed with chunk 4's K/V
+    for c in (0, 1, 2, 4):
+        wb.append(*kv[c])
+    assert torch.equal(wa.pool, wb.pool)
+    outs = []
+    for w in (wa, wb):
+        w.build_topk_lists(q, 2)
+        lists = [t.clone() for t in w.lists_views()]
+        o, lse = w.attention(q)
+        torch.cuda.synchronize()
+        outs.append((lists, o, lse))
+    for a, b in zip(outs[0][0], outs[1][0]):
+        assert torch.equal(a, b)
+    assert torch.equal(outs[0][1], outs[1][1]) and torch.equal(outs[0][2], outs[1][2])

@@ -34,7 +34,7 @@ def _declared():
 def test_library_exports_every_declared_symbol(P):
     from paper_2606_09150_amd import _lib
     names = _declared()
-    assert len(names) == 15
+    assert len(names) == 16
     lib = ctypes.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -212,3 +212,17 @@ def test_topk_host_paths(P):
     for args in ((-1.0, 1, 1, 1, 0), (float("nan"), 1, 1, 1, 0), (1.0, 1, 0, 1, 0), (1.0, -1, 1, 1, 0),
                  (1.0, 1, 1, 1, -1)):
         assert status(L.uf_topk_budget, *args) == L.UF_ERR_ARG
+
+
+def test_replace_newest_keeps_window_metadata(P):
+    L = P._lib
+    w = _dry(P, max_chunks=3)
+    with pytest.raises(P.UfError) as ei:
+        w.replace_newest(None, None)
+    assert ei.value.status == L.UF_ERR_EMPTY
+    for _ in range(3):
+        w.append(None, None)
+    before = [w.logical(p) for p in range(3)], (w.info().first_seq, w.info().last_seq, w.info().n_live)
+    w.replace_newest(None, None)
+    after = [w.logical(p) for p in range(3)], (w.info().first_seq, w.info().last_seq, w.info().n_live)
+    assert before == after
