@@ -86,7 +86,7 @@ def _flops_of_lists(win, lists, nt, tail, T):
     return kept, padded
 
 
-def run_workload(P, wl, steps, warmup, n_src=3):
+def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     import torch
     import synth
 
@@ -105,6 +105,9 @@ def run_workload(P, wl, steps, warmup, n_src=3):
     out = torch.empty((B, L, H, D), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
+    work = None
+    if split:
+        work = torch.empty(P.uf_attn_split_work_bytes(win.handle, split), dtype=torch.uint8, device=dev)
     scale = 1.0 / math.sqrt(D)
     stream = torch.cuda.current_stream(dev)
 
@@ -119,7 +122,7 @@ def run_workload(P, wl, steps, warmup, n_src=3):
         win.lists = lists[s]
         win.build_lists(wl.seed, wl.p_prior)
         e[2].record(stream)
-        win.attention(src["q"], scale, out=out, lse=lse)
+        win.attention(src["q"], scale, out=out, lse=lse, split=split, work=work)
         e[3].record(stream)
 
     for s in range(warmup):
@@ -282,6 +285,8 @@ def main():
     ap.add_argument("--secondary", default="2k", help="second workload reported in the same line ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--split", type=int, default=0,
+                    help="split-KV attention with this many list slices per row (0: whole rows)")
     ap.add_argument("--sweep", action="store_true",
                     help="also time the attention against sparsity (top-k lists, no forced chunks)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -306,7 +311,9 @@ def main():
         sys.exit(1)
 
     wl = synth.WORKLOADS[args.config]
-    res, state = run_workload(P, wl, args.steps, args.warmup)
+    res, state = run_workload(P, wl, args.steps, args.warmup, split=args.split)
+    if args.split:
+        res["split"] = args.split
     line = {
         "metric": METRIC,
         "value": res["value"],
@@ -326,6 +333,8 @@ def main():
                    "window_chunks": wl.window_chunks, "keys": res["keys"], "p_prior": wl.p_prior,
                    "pinned_first_chunk": wl.pin_sink},
     }
+    for k in ("split",) if args.split else ():
+        line[k] = res[k]
     for k in ("attn_ms", "attn_ms_p10", "attn_ms_p90", "attn_tflops", "append_us", "append_gbps", "lists_us",
               "topk_budget", "topk_lists_us", "kept_tflop_per_step", "kept_fraction", "padded_tile_tflop_per_step"):
         line[k] = res[k]

@@ -59,6 +59,7 @@ extern "C" {
                                instead of 0 (checks that padding never counts) */
 
 #define UF_MAX_CHUNKS 64    /* largest window capacity */
+#define UF_MAX_SPLIT  64    /* largest split-KV slice count */
 
 typedef struct uf_kv uf_kv; /* opaque host-side handle of one KV window */
 
@@ -238,6 +239,21 @@ int uf_topk_budget(double rho, int64_t seq_len, int64_t seq_ref, int64_t n_block
  * UF_ERR_EMPTY, UF_ERR_HIP. */
 int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists,
                               float scale, void* d_o, float* d_lse, void* stream);
+
+/* Split-KV attention (for windows whose rows are too few to fill the GPU):
+ * the same operation as uf_sparse_causal_attn_fwd, with the kept-tile list of
+ * every row cut into n_split contiguous slices (slice s takes entries
+ * [s*count/n_split, (s+1)*count/n_split)) that separate workgroups attend;
+ * each slice leaves its unnormalised output, running offset and row sum in
+ * d_work, and a merge combines them by the same log-sum-exp rescaling as the
+ * online softmax.  d_work (16-byte aligned, >= uf_attn_split_work_bytes) is
+ * caller-owned scratch, overwritten.  Needs 128-token tiles.  Results equal
+ * those of uf_sparse_causal_attn_fwd up to float rounding order.  Errors:
+ * UF_ERR_ARG, UF_ERR_UNSUPPORTED (tile 64), UF_ERR_EMPTY, UF_ERR_HIP. */
+int uf_attn_split_work_bytes(const uf_kv* kv, int32_t n_split, size_t* bytes);
+int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
+                                    void* d_o, float* d_lse, int32_t n_split, void* d_work,
+                                    size_t work_bytes, void* stream);
 
 /* Static text of a status code. */
 const char* uf_status_string(int status);

@@ -195,11 +195,16 @@ __device__ __forceinline__ void pp_softmax(PPState& st, int valid, int hl, float
   st.l += rs;
 }
 
+// SPLIT: workgroup (row, s) of a split-KV launch takes list entries
+// [s*count/split, (s+1)*count/split) of its row and writes its unnormalised
+// partial (O relative to its offset m, and l) to a.work; a merge combines them.
+template <bool SPLIT>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   __shared__ uint4 sK[2][kT * 16];   // two K tiles: 128 key rows x 16 chunks
   __shared__ uint4 sV[3][kD * 16];   // three V^T tiles: 128 dim rows x 16 chunks
 
-  const int row = blockIdx.x;
+  const int row = SPLIT ? int(blockIdx.x) / a.split : int(blockIdx.x);
+  const int part = SPLIT ? int(blockIdx.x) - row * a.split : 0;
   const int qt = row % a.NT;
   const int bh = row / a.NT;
   const int h = bh % a.H;
@@ -250,10 +255,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   const size_t pbytes = page_bytes(kT, kD);
   const uint8_t* head_pages = a.pool + (size_t(b) * a.H + h) * a.NT * pbytes;
   const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
-  const int count = ((const const_i32*)a.counts)[row];
+  const int total = ((const const_i32*)a.counts)[row];
+  const int first = SPLIT ? int(int64_t(part) * total / a.split) : 0;
+  const int count = SPLIT ? int(int64_t(part + 1) * total / a.split) - first : total;
   const float c2 = a.scale_log2;
   const int N = count;
-  const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
+  const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap + first;
 
   // Page of list entry n and its valid keys.  An entry naming a tile outside
   // the window (stale lists) reads a page of this head and counts no key.
@@ -393,6 +400,29 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     const float fa = (st.m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(st.m - mm);
     const float fb = (mB == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mB - mm);
     const float l = st.l * fa + lB * fb;
+    if (SPLIT) {
+      if (qvalid) {
+        const size_t wrow = size_t(row) * a.split + part;
+        float* op = a.work + (wrow * kT + qw * 32 + ln) * kD;
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int d0 = mb * 32 + 8 * i + 4 * hl;
+            float4 v;
+            v.x = st.o[mb][4 * i + 0] * fa + xo[((qw * 4 + mb) * 16 + 4 * i + 0) * 64 + lane] * fb;
+            v.y = st.o[mb][4 * i + 1] * fa + xo[((qw * 4 + mb) * 16 + 4 * i + 1) * 64 + lane] * fb;
+            v.z = st.o[mb][4 * i + 2] * fa + xo[((qw * 4 + mb) * 16 + 4 * i + 2) * 64 + lane] * fb;
+            v.w = st.o[mb][4 * i + 3] * fa + xo[((qw * 4 + mb) * 16 + 4 * i + 3) * 64 + lane] * fb;
+            *reinterpret_cast<float4*>(op + d0) = v;
+          }
+        if (hl == 0) {
+          float2* ml = reinterpret_cast<float2*>(a.work + size_t(a.B) * a.H * a.NT * a.split * kT * kD);
+          ml[wrow * kT + qw * 32 + ln] = make_float2(mm, l);
+        }
+      }
+      return;
+    }
     if (qvalid) {
       const float inv = (l > 0.f) ? 1.f / l : 0.f;
       const float wa = fa * inv, wb = fb * inv;
@@ -417,11 +447,73 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
   }
 }
 
+// Split-KV merge: one workgroup per row; lane (query, half) combines the
+// row's partials for 64 dims: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+__global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
+  const int row = blockIdx.x;
+  const int qt = row % a.NT;
+  const int bh = row / a.NT;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
+  const int ql = threadIdx.x >> 1;
+  const int half = threadIdx.x & 1;
+  const int qrow = qt * kT + ql;
+  if (qrow >= a.L) return;
+  const float2* ml = reinterpret_cast<const float2*>(a.work + size_t(a.B) * a.H * a.NT * a.split * kT * kD);
+  float mm = -INFINITY;
+  for (int s = 0; s < a.split; ++s) {
+    const float2 v = ml[(size_t(row) * a.split + s) * kT + ql];
+    if (v.y > 0.f) mm = fmaxf(mm, v.x);
+  }
+  float acc[64];
+#pragma unroll
+  for (int d = 0; d < 64; ++d) acc[d] = 0.f;
+  float l = 0.f;
+  for (int s = 0; s < a.split; ++s) {
+    const size_t wrow = size_t(row) * a.split + s;
+    const float2 v = ml[wrow * kT + ql];
+    if (!(v.y > 0.f)) continue;   // empty slice
+    const float w = __builtin_amdgcn_exp2f(v.x - mm);
+    l += v.y * w;
+    const float4* op = reinterpret_cast<const float4*>(a.work + (wrow * kT + ql) * kD + 64 * half);
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const float4 o = op[c];
+      acc[4 * c + 0] += o.x * w;
+      acc[4 * c + 1] += o.y * w;
+      acc[4 * c + 2] += o.z * w;
+      acc[4 * c + 3] += o.w * w;
+    }
+  }
+  const float inv = (l > 0.f) ? 1.f / l : 0.f;
+  uint16_t* out = a.o + ((size_t(b) * a.L + qrow) * a.H + h) * kD + 64 * half;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    uint4 w;
+    w.x = pack_bf16x2(acc[8 * c + 0] * inv, acc[8 * c + 1] * inv);
+    w.y = pack_bf16x2(acc[8 * c + 2] * inv, acc[8 * c + 3] * inv);
+    w.z = pack_bf16x2(acc[8 * c + 4] * inv, acc[8 * c + 5] * inv);
+    w.w = pack_bf16x2(acc[8 * c + 6] * inv, acc[8 * c + 7] * inv);
+    reinterpret_cast<uint4*>(out)[c] = w;
+  }
+  if (a.lse != nullptr && half == 0)
+    a.lse[(size_t(b) * a.H + h) * a.L + qrow] = (l > 0.f) ? (mm + log2f(l)) * 0.69314718055994531f : -INFINITY;
+}
+
 }  // namespace
 
 hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
-  attn_fwd_pp_kernel<<<blocks, kThreads, 0, stream>>>(a);
+  attn_fwd_pp_kernel<false><<<blocks, kThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_fwd_t128_pp_split(const AttnArgs& a, hipStream_t stream) {
+  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
+  attn_fwd_pp_kernel<true><<<rows * unsigned(a.split), kThreads, 0, stream>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  attn_split_merge_kernel<<<rows, 256, 0, stream>>>(a);
   return hipGetLastError();
 }
 

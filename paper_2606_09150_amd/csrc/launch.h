@@ -69,11 +69,14 @@ struct AttnArgs {
   int32_t B, H, L, T, NT, tail, nk, nk_cap;
   float scale;            // softmax scale
   float scale_log2;       // scale * log2(e)
+  int32_t split;          // list slices per row (split-KV), 1 = whole rows
+  float* work;            // split-KV partials: O [rows*split][T][D], then (m, l) [rows*split][T]
   int32_t slot_of[UF_MAX_CHUNKS];  // slot of each logical position
 };
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_w32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t128_pp_split(const AttnArgs& a, hipStream_t stream);
 
 inline hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   return a.T == 128 ? launch_attn_fwd_t128_pp(a, stream) : launch_attn_fwd_t64(a, stream);

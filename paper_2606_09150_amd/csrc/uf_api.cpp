@@ -339,13 +339,16 @@ int uf_topk_budget(double rho, int64_t seq_len, int64_t seq_ref, int64_t n_block
   return ok();
 }
 
-int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
-                              void* d_o, float* d_lse, void* stream) {
+namespace {
+
+// Validation and arguments shared by the attention entry points.
+int attn_args(const uf_kv* kv, const void* d_q, const void* d_lists, float scale, void* d_o, float* d_lse,
+              uf::AttnArgs* out) {
   if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
   if (!(std::isfinite(scale) && scale > 0.f && std::isnormal(scale * 1.4426950408889634f)))
     return fail(UF_ERR_ARG, "scale must be positive, finite and normal");
   if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
-  if (kv->dry()) return ok();
+  if (kv->dry()) return UF_OK;
   if (d_q == nullptr || d_o == nullptr || d_lists == nullptr) return fail(UF_ERR_ARG, "q, o or lists is null");
   if (!aligned(d_q, 16) || !aligned(d_o, 16)) return fail(UF_ERR_ARG, "q and o must be 16-byte aligned");
   if (!aligned(d_lists, 256)) return fail(UF_ERR_ARG, "lists must be 256-byte aligned");
@@ -368,9 +371,54 @@ int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_li
   a.nk_cap = kv->nk_cap;
   a.scale = scale;
   a.scale_log2 = scale * 1.4426950408889634f;
+  a.split = 1;
+  a.work = nullptr;
   for (size_t p = 0; p < kv->live.size(); ++p) a.slot_of[p] = kv->live[p].slot;
+  *out = a;
+  return UF_OK;
+}
+
+size_t split_work_bytes(const uf_kv* kv, int32_t n_split) {
+  const size_t rows = size_t(kv->layout().rows);
+  return rows * size_t(n_split) * size_t(kv->d.tile) * (size_t(kv->d.head_dim) + 2) * 4;
+}
+
+}  // namespace
+
+int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
+                              void* d_o, float* d_lse, void* stream) {
+  uf::AttnArgs a{};
+  if (int s = attn_args(kv, d_q, d_lists, scale, d_o, d_lse, &a)) return s;
+  if (kv->dry()) return ok();
   hipError_t e = uf::launch_attn_fwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_attn_split_work_bytes(const uf_kv* kv, int32_t n_split, size_t* bytes) {
+  if (kv == nullptr || bytes == nullptr) return fail(UF_ERR_ARG, "null argument");
+  if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
+  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
+  *bytes = split_work_bytes(kv, n_split);
+  return ok();
+}
+
+int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
+                                    void* d_o, float* d_lse, int32_t n_split, void* d_work, size_t work_bytes,
+                                    void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
+  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
+  uf::AttnArgs a{};
+  if (int s = attn_args(kv, d_q, d_lists, scale, d_o, d_lse, &a)) return s;
+  if (kv->dry()) return ok();
+  if (d_work == nullptr || !aligned(d_work, 16)) return fail(UF_ERR_ARG, "work must be non-null and 16-byte aligned");
+  if (work_bytes < split_work_bytes(kv, n_split))
+    return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, split_work_bytes(kv, n_split));
+  a.split = n_split;
+  a.work = static_cast<float*>(d_work);
+  hipError_t e = uf::launch_attn_fwd_t128_pp_split(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));
   return ok();
 }
 

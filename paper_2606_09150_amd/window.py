@@ -116,8 +116,11 @@ class KVWindow:
         return counts, idx, mask
 
     # -- attention ----------------------------------------------------------
-    def attention(self, q, scale=None, out=None, lse=True, lists=None, stream=None):
-        """O [B,L,H,D] bf16 (and LSE [B,H,L] fp32 when ``lse``) for the current chunk."""
+    def attention(self, q, scale=None, out=None, lse=True, lists=None, stream=None, split=None, work=None):
+        """O [B,L,H,D] bf16 (and LSE [B,H,L] fp32 when ``lse``) for the current chunk.
+
+        ``split`` > 0 selects split-KV attention with that many list slices per
+        row; ``work`` is its scratch buffer (allocated here when None)."""
         _check_chunk(q, "q", self.B, self.L, self.H, self.D)
         if scale is None:
             scale = 1.0 / math.sqrt(self.D)
@@ -135,5 +138,11 @@ class KVWindow:
         buf = self.lists if lists is None else lists
         if buf.numel() < self.layout.total_bytes:
             raise ValueError("list buffer too small")
-        L.uf_sparse_causal_attn_fwd(self.handle, q, buf, scale, out, lse_t, stream)
+        if split:
+            need = L.uf_attn_split_work_bytes(self.handle, int(split))
+            if work is None:
+                work = torch.empty(need, dtype=torch.uint8, device=q.device)
+            L.uf_sparse_causal_attn_fwd_split(self.handle, q, buf, scale, out, lse_t, int(split), work, None, stream)
+        else:
+            L.uf_sparse_causal_attn_fwd(self.handle, q, buf, scale, out, lse_t, stream)
         return (out, lse_t) if lse_t is not None else out

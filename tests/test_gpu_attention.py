@@ -282,3 +282,64 @@ def test_lse_optional_and_outputs_untouched_beyond_shape():
     assert (big[:, 200:] == 7.0).all()
     o2, _ = case.attention(q)
     assert torch.equal(o1, o2)
+
+
+@pytest.mark.parametrize("n_split", [1, 2, 3, 7])
+def test_split_kv_parity(n_split):
+    """Split-KV: list slices attended by separate workgroups and merged; the oracle's
+    bar, and agreement with the unsplit kernel up to rounding order."""
+    P = require_gpu()
+    log(f"attn split n_split={n_split}")
+    case = Case(P, 2, 700, 3, 128, 5, True, seed=77)
+    for _ in range(6):
+        case.append()
+    rule = case.rule(0.5)
+    case.gpu_lists(rule)
+    q = case.query()
+    o1, l1 = case.attention(q)
+    os_, ls_ = case.win.attention(q, split=n_split)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(os_), O)
+    lerr = float(np.abs(f64(ls_) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= LSE_TOL
+    assert row_rel_err(case._host(os_), case._host(o1)) <= REL_TOL
+    assert float((ls_ - l1).abs().max()) <= LSE_TOL
+
+
+def test_split_kv_more_slices_than_tiles():
+    """Rows with fewer kept tiles than slices leave empty slices, which the merge skips."""
+    P = require_gpu()
+    case = Case(P, 1, 200, 2, 128, 3, True, seed=78)
+    for _ in range(3):
+        case.append()
+    rule = case.rule(0.3)
+    case.gpu_lists(rule)
+    q = case.query()
+    o, lse = case.win.attention(q, split=64)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
+    assert row_rel_err(case._host(o), O) <= REL_TOL
+    assert float(np.abs(f64(lse) - LSE).max()) <= LSE_TOL
+
+
+def test_split_kv_480p_full():
+    P = require_gpu()
+    log("attn split 480p full, n_split=4")
+    wl, case = _workload_case(P, "480p", "cuda")
+    for _ in range(wl.window_chunks):
+        case.append()
+    rule = case.rule(wl.p_prior)
+    case.gpu_lists(rule)
+    q = case.query()
+    o, lse = case.win.attention(q, split=4)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, wl.tile, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(o), O)
+    lerr = float(np.abs(f64(lse) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= LSE_TOL

@@ -34,7 +34,7 @@ def _declared():
 def test_library_exports_every_declared_symbol(P):
     from paper_2606_09150_amd import _lib
     names = _declared()
-    assert len(names) == 16
+    assert len(names) == 18
     lib = ctypes.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -226,3 +226,28 @@ def test_replace_newest_keeps_window_metadata(P):
     w.replace_newest(None, None)
     after = [w.logical(p) for p in range(3)], (w.info().first_seq, w.info().last_seq, w.info().n_live)
     assert before == after
+
+
+def test_split_kv_host_paths(P):
+    L = P._lib
+    E = P.UfError
+
+    def status(fn, *a):
+        with pytest.raises(E) as ei:
+            fn(*a)
+        return ei.value.status
+
+    w = _dry(P, max_chunks=4, L=300, T=128, H=2)
+    rows = 2 * 3
+    assert L.uf_attn_split_work_bytes(w.handle, 4) == rows * 4 * 128 * 130 * 4
+    for n in (0, -1, 65):
+        assert status(L.uf_attn_split_work_bytes, w.handle, n) == L.UF_ERR_ARG
+    assert status(L.uf_sparse_causal_attn_fwd_split, w.handle, None, None, 0.1, None, None, 2, None, 0) == L.UF_ERR_EMPTY
+    w.append(None, None)
+    L.uf_sparse_causal_attn_fwd_split(w.handle, None, None, 0.1, None, None, 2, None, 0)   # dry run
+    assert status(L.uf_sparse_causal_attn_fwd_split, w.handle, None, None, 0.1, None, None, 0, None, 0) == L.UF_ERR_ARG
+    w64 = _dry(P, max_chunks=2, L=300, T=64)
+    w64.append(None, None)
+    assert status(L.uf_attn_split_work_bytes, w64.handle, 2) == L.UF_ERR_UNSUPPORTED
+    assert status(L.uf_sparse_causal_attn_fwd_split, w64.handle, None, None, 0.1, None, None, 2, None, 0) == \
+        L.UF_ERR_UNSUPPORTED
