@@ -22,6 +22,9 @@ It is a plain, slow, obviously correct restatement of what the method computes
                    query and key tiles, block scores, top-k per (head, query
                    tile) with forced pinned/current chunks; fixed float32
                    arithmetic (parity against the paper unpinned).
+* ``blocks``    -- the 3-D (b_t, b_h, b_w) block tiling of a chunk's token
+                   grid, the block order of tokens, the r x r local window
+                   mask M_local, and attention evaluated in raster order.
 * ``attention`` -- softmax attention of the current chunk's queries over the
                    union of kept key tiles (Eq. 4 mask semantics), computed as
                    masked dense attention in float64.
@@ -49,6 +52,14 @@ from .topk import (
     topk_scores,
     topk_bits,
 )
+from .blocks import (
+    BlockGeom,
+    block_order,
+    block_of_token,
+    block_means,
+    local_mask,
+    attention_in_raster,
+)
 from .attention import (
     sparse_causal_attention,
     sparse_causal_attention_rows,
@@ -65,6 +76,12 @@ __all__ = [
     "tile_geometry",
     "keep_bits",
     "lists_from_bits",
+    "BlockGeom",
+    "block_order",
+    "block_of_token",
+    "block_means",
+    "local_mask",
+    "attention_in_raster",
     "TopkRule",
     "topk_budget",
     "pooled_means",
