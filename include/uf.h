@@ -93,6 +93,9 @@ typedef struct {
   double p_prior;       /* in [0, 1]; 1 keeps every tile (dense) */
   int32_t keep_sink;    /* 0 or 1 */
   int32_t keep_current; /* 0 or 1 */
+  int32_t local_r;      /* 0: no local mask; odd r >= 1: intersect with M_local
+                           (needs block geometry, see uf_kv_set_block_geom) */
+  int32_t reserved;     /* must be 0 */
 } uf_keep_rule;
 
 /* Content-adaptive top-k rule for uf_build_topk_lists (Sec. 2.3.1 (b), Eq. 4).
@@ -114,7 +117,8 @@ typedef struct {
   int32_t budget;       /* k >= 0: ranked tiles kept per row (all if k >= candidates) */
   int32_t keep_sink;    /* 0 or 1 */
   int32_t keep_current; /* 0 or 1 */
-  int32_t reserved;     /* must be 0 */
+  int32_t local_r;      /* 0: no local mask; odd r >= 1: intersect the kept set
+                           with M_local (needs block geometry) */
 } uf_topk_rule;
 
 typedef struct {
@@ -186,6 +190,47 @@ int uf_kv_append(uf_kv* kv, const void* d_k, const void* d_v, void* stream);
  * enqueued on the same stream happen first.  Errors: UF_ERR_ARG, UF_ERR_EMPTY
  * (no chunk), UF_ERR_HIP. */
 int uf_kv_replace_newest(uf_kv* kv, const void* d_k, const void* d_v, void* stream);
+
+/* 3-D block tiling of a chunk's token grid (Sec. 2.3.1 (a): the (t, h, w) grid
+ * divided into non-overlapping (bt, bh, bw) blocks; (2, 8, 8) in the paper).
+ * A chunk of `frames` latent frames on a grid_h x grid_w grid has blocks
+ * (ceil(frames/bt), ceil(grid_h/bh), ceil(grid_w/bw)) in raster order (block
+ * time, block row, block column).  In block order a chunk holds one tile of
+ * bt*bh*bw rows per block: the block's valid tokens in raster (t, h, w) order,
+ * then padding rows that count as no token.  With block geometry the local
+ * window M_local(r) keeps key block j for query block i iff their block rows
+ * and block columns differ by at most r/2 (integer division), in every chunk
+ * and at every block time; it is intersected with the keep rule (forced
+ * tiles included), as Eq. 4 intersects the content mask with the structural
+ * ones. */
+typedef struct {
+  int32_t frames, grid_h, grid_w;
+  int32_t bt, bh, bw;
+} uf_block_geom;
+
+#define UF_MAX_BLOCKS 2048  /* blocks per chunk under block geometry */
+
+/* Tokens of a chunk in block order (blocks * bt*bh*bw) and its block count.
+ * Errors: UF_ERR_ARG (null, non-positive field), UF_ERR_UNSUPPORTED (more
+ * than UF_MAX_BLOCKS blocks). */
+int uf_block_geom_tokens(const uf_block_geom* g, int32_t* padded_tokens, int32_t* n_blocks);
+
+/* Give an empty window block geometry: its tiles become blocks (tile must be
+ * bt*bh*bw and chunk_tokens the padded block-order length); append, the list
+ * builders and attention then count a tile's valid rows from the geometry and
+ * the rules may use M_local.  K, V and Q are passed in block order (see
+ * uf_block_permute).  Errors: UF_ERR_ARG (bad geometry, mismatched tile or
+ * chunk length, window not empty), UF_ERR_UNSUPPORTED (too many blocks). */
+int uf_kv_set_block_geom(uf_kv* kv, const uf_block_geom* g);
+
+/* Reorder [batch, tokens, heads, head_dim] bf16 rows between raster order
+ * (frames*grid_h*grid_w tokens) and block order (padded block-order tokens):
+ * inverse = 0 writes block order from raster (padding rows zero), inverse = 1
+ * writes raster order from block order (padding rows dropped).  Buffers
+ * 16-byte aligned, not overlapping; head_dim must be 128.  Errors: UF_ERR_ARG,
+ * UF_ERR_UNSUPPORTED, UF_ERR_HIP. */
+int uf_block_permute(const uf_block_geom* g, int32_t batch, int32_t heads, int32_t head_dim,
+                     const void* d_src, void* d_dst, int32_t inverse, void* stream);
 
 /* Drop the n oldest chunks that are not pinned (Sec. 2.3.2 (iii): a compact
  * cache window).  Host metadata only: the freed slot is rewritten by a later

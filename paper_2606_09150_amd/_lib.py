@@ -36,12 +36,18 @@ class uf_kv_desc(ctypes.Structure):
 
 class uf_keep_rule(ctypes.Structure):
     _fields_ = [("seed", ctypes.c_uint64), ("p_prior", ctypes.c_double),
-                ("keep_sink", ctypes.c_int32), ("keep_current", ctypes.c_int32)]
+                ("keep_sink", ctypes.c_int32), ("keep_current", ctypes.c_int32),
+                ("local_r", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class uf_block_geom(ctypes.Structure):
+    _fields_ = [("frames", ctypes.c_int32), ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32),
+                ("bt", ctypes.c_int32), ("bh", ctypes.c_int32), ("bw", ctypes.c_int32)]
 
 
 class uf_topk_rule(ctypes.Structure):
     _fields_ = [("budget", ctypes.c_int32), ("keep_sink", ctypes.c_int32),
-                ("keep_current", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("keep_current", ctypes.c_int32), ("local_r", ctypes.c_int32)]
 
 
 class uf_kv_info(ctypes.Structure):
@@ -65,6 +71,11 @@ _SIGNATURES = {
     "uf_kv_destroy": (ctypes.c_int, [_P]),
     "uf_kv_append": (ctypes.c_int, [_P, _P, _P, _P]),
     "uf_kv_evict": (ctypes.c_int, [_P, ctypes.c_int32]),
+    "uf_block_geom_tokens": (ctypes.c_int, [ctypes.POINTER(uf_block_geom), ctypes.POINTER(ctypes.c_int32),
+                                            ctypes.POINTER(ctypes.c_int32)]),
+    "uf_kv_set_block_geom": (ctypes.c_int, [_P, ctypes.POINTER(uf_block_geom)]),
+    "uf_block_permute": (ctypes.c_int, [ctypes.POINTER(uf_block_geom), ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_int32, _P, _P, ctypes.c_int32, _P]),
     "uf_kv_replace_newest": (ctypes.c_int, [_P, _P, _P, _P]),
     "uf_kv_get_info": (ctypes.c_int, [_P, ctypes.POINTER(uf_kv_info)]),
     "uf_kv_logical": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
@@ -159,6 +170,22 @@ def uf_kv_append(handle, k, v, stream=None) -> None:
 def uf_kv_replace_newest(handle, k, v, stream=None) -> None:
     s = None if k is None else _stream_ptr(stream)
     _check(load().uf_kv_replace_newest(handle, _ptr(k), _ptr(v), s))
+
+
+def uf_block_geom_tokens(geom: uf_block_geom):
+    padded, nb = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(load().uf_block_geom_tokens(ctypes.byref(geom), ctypes.byref(padded), ctypes.byref(nb)))
+    return padded.value, nb.value
+
+
+def uf_kv_set_block_geom(handle, geom: uf_block_geom) -> None:
+    _check(load().uf_kv_set_block_geom(handle, ctypes.byref(geom)))
+
+
+def uf_block_permute(geom: uf_block_geom, batch: int, heads: int, src, dst, inverse: int, head_dim: int = 128,
+                     stream=None) -> None:
+    s = None if src is None else _stream_ptr(stream)
+    _check(load().uf_block_permute(ctypes.byref(geom), batch, heads, head_dim, _ptr(src), _ptr(dst), int(inverse), s))
 
 
 def uf_kv_evict(handle, n_chunks: int) -> None:

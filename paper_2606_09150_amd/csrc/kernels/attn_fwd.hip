@@ -141,7 +141,7 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
     const int nn = next_valid(n + 1);
     const bool has_next = nn < count;
     const int t_cur = list[n] % a.NT;
-    const int valid = (t_cur == a.NT - 1) ? a.tail : T;
+    const int valid = tile_valid(a.tv, t_cur, a.NT, a.tail, T);
     const uint8_t* pnext = has_next ? page_of(nn) : nullptr;
 
     // K_n has landed once only V_n's loads may still be outstanding.

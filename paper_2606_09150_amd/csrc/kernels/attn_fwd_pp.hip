@@ -272,7 +272,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_pp_kernel(AttnArgs a) {
     }
     const int pos = j / a.NT;
     const int t = j - pos * a.NT;
-    valid = (t == a.NT - 1) ? a.tail : kT;
+    valid = tile_valid(a.tv, t, a.NT, a.tail, kT);
     return head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
   };
   // Copy jobs: K tile n into K buffer n % 2, V tile n into V buffer n % 3.

@@ -31,7 +31,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a) {
   const int bh = page / a.NT;
   const int h = bh % a.H;
   const int b = bh / a.H;
-  const int valid = (t == a.NT - 1) ? a.tail : T;
+  const int valid = tile_valid(a.tv, t, a.NT, a.tail, T);
 
   uint8_t* dst = a.pool + (size_t(a.slot) * a.B * a.H * a.NT + size_t(page)) * page_bytes(T, kD);
   uint4 pad;

@@ -48,6 +48,7 @@ __global__ __launch_bounds__(kThreads) void tile_lists_kernel(ListArgs a) {
     if (j >= a.nk) return false;
     const int pos = j / a.NT;
     const int t = j - pos * a.NT;
+    if (!tile_local(a.tv, i, t)) return false;   // structural local window (block geometry)
     if ((a.sink[pos] && a.keep_sink) || (a.seq[pos] == a.cur_seq && a.keep_current)) return true;
     uint64_t y = splitmix64(x ^ uint64_t(a.seq[pos]));
     y = splitmix64(y ^ uint64_t(t));

@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kThreads) void pool_queries_kernel(TopkArgs a) {
   const int bh = row / a.NT;
   const int h = bh % a.H;
   const int b = bh / a.H;
-  const int nv = (i == a.NT - 1) ? a.tail : T;
+  const int nv = tile_valid(a.tv, i, a.NT, a.tail, T);
   for (int c = threadIdx.x; c < nv * (kD / 8); c += kThreads) {
     const int r = c / (kD / 8);
     const int cc = c - r * (kD / 8);
@@ -202,9 +202,11 @@ __global__ __launch_bounds__(kThreads) void topk_lists_kernel(TopkArgs a) {
     int32_t* idx = reinterpret_cast<int32_t*>(a.lists + a.idx_offset) + size_t(row) * a.nk_cap;
     uint32_t* mask = reinterpret_cast<uint32_t*>(a.lists + a.mask_offset) + size_t(row) * a.mask_words;
     const uint8_t* sg = sel + size_t(g) * nc;
+    const int qi = i0 + g;
     auto keep_of = [&](int j) {
       if (j >= a.nk) return false;
-      if (j < a.cand_lo || j >= a.cand_hi) return true;   // forced: pinned or current chunk
+      if (!tile_local(a.tv, qi, j % a.NT)) return false;   // structural local window (block geometry)
+      if (j < a.cand_lo || j >= a.cand_hi) return true;    // forced: pinned or current chunk
       return sg[j - a.cand_lo] != 0;
     };
     lists::emit_row(keep_of, a.nk_cap, a.mask_words, counts + row, idx, mask, wave_count);

@@ -19,6 +19,25 @@ __host__ __device__ inline int swap23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
+// Valid rows of the tiles of a chunk: the last tile holds `tail` rows, unless
+// the window has block geometry, whose per-block counts are tabulated.
+struct TileValid {
+  int32_t blocked;                 // 0: raster tiles
+  int32_t nbh, nbw;                // block rows and columns of the grid (blocked)
+  int32_t local_half;              // M_local half-width in blocks, -1: no local mask
+  uint8_t count[UF_MAX_BLOCKS];    // valid rows of tile t (blocked)
+};
+__host__ __device__ inline int tile_valid(const TileValid& v, int t, int NT, int tail, int T) {
+  return v.blocked ? int(v.count[t]) : ((t == NT - 1) ? tail : T);
+}
+// M_local between query tile i and key tile t (block indices of one chunk).
+__host__ __device__ inline bool tile_local(const TileValid& v, int i, int t) {
+  if (v.local_half < 0) return true;
+  const int dh = (i / v.nbw) % v.nbh - (t / v.nbw) % v.nbh;
+  const int dw = i % v.nbw - t % v.nbw;
+  return (dh <= v.local_half && -dh <= v.local_half) && (dw <= v.local_half && -dw <= v.local_half);
+}
+
 struct AppendArgs {
   const uint16_t* k;      // [B, L, H, D]
   const uint16_t* v;      // [B, L, H, D]
@@ -27,6 +46,7 @@ struct AppendArgs {
   int64_t slot;
   int32_t B, H, L, T, NT, tail;
   uint16_t pad;           // bf16 bits written into padding rows
+  TileValid tv;
 };
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t stream);
 
@@ -41,6 +61,7 @@ struct ListArgs {
   int64_t cur_seq;
   int64_t seq[UF_MAX_CHUNKS];   // per logical position
   int32_t sink[UF_MAX_CHUNKS];  // 1 if logical position holds the pinned chunk
+  TileValid tv;
 };
 hipError_t launch_tile_lists(const ListArgs& a, hipStream_t stream);
 
@@ -55,6 +76,7 @@ struct TopkArgs {
   int32_t cand_lo, cand_hi;   // ranked logical tiles [cand_lo, cand_hi)
   int32_t budget;
   int32_t slot_of[UF_MAX_CHUNKS];
+  TileValid tv;
 };
 constexpr int kTopkMaxCandidates = 16384;   // G * candidates per workgroup
 hipError_t launch_topk_lists(const TopkArgs& a, size_t lds_bytes, hipStream_t stream);
@@ -72,7 +94,16 @@ struct AttnArgs {
   int32_t split;          // list slices per row (split-KV), 1 = whole rows
   float* work;            // split-KV partials: O [rows*split][T][D], then (m, l) [rows*split][T]
   int32_t slot_of[UF_MAX_CHUNKS];  // slot of each logical position
+  TileValid tv;
 };
+
+// Block-order permutation of [B, tokens, H, 128] bf16 rows.
+struct PermuteArgs {
+  const uint16_t* src;
+  uint16_t* dst;
+  int32_t B, H, frames, gh, gw, bt, bh, bw, nbh, nbw, tokens, padded, inverse;
+};
+hipError_t launch_block_permute(const PermuteArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_w32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream);

@@ -70,6 +70,20 @@ int check_desc(const uf_kv_desc* d) {
 struct uf_kv {
   uf_kv_desc d;
   uint8_t* pool;
+  // block geometry (uf_kv_set_block_geom): tiles are 3-D blocks
+  bool blocked = false;
+  uf_block_geom geom{};
+  int32_t nbh = 0, nbw = 0;
+  uint8_t block_valid[UF_MAX_BLOCKS] = {};
+  uf::TileValid tile_valid(int32_t local_r) const {
+    uf::TileValid v{};
+    v.blocked = blocked ? 1 : 0;
+    v.nbh = blocked ? nbh : 1;
+    v.nbw = blocked ? nbw : 1;
+    v.local_half = (blocked && local_r > 0) ? local_r / 2 : -1;
+    if (blocked) std::memcpy(v.count, block_valid, sizeof(block_valid));
+    return v;
+  }
   // pooled keys follow the pages: [max_chunks][B][H][NT][D] float32
   float* kmean() const {
     const size_t pages = size_t(d.max_chunks) * d.batch * d.heads * nt;
@@ -100,6 +114,32 @@ struct uf_kv {
     return lay;
   }
 };
+
+namespace {
+
+int check_geom(const uf_block_geom* g, int32_t* padded, int32_t* nblocks) {
+  if (g == nullptr) return fail(UF_ERR_ARG, "geometry is null");
+  if (g->frames < 1 || g->grid_h < 1 || g->grid_w < 1 || g->bt < 1 || g->bh < 1 || g->bw < 1)
+    return fail(UF_ERR_ARG, "geometry fields must be >= 1");
+  const int64_t nb = int64_t((g->frames + g->bt - 1) / g->bt) * ((g->grid_h + g->bh - 1) / g->bh) *
+                     ((g->grid_w + g->bw - 1) / g->bw);
+  const int64_t tile = int64_t(g->bt) * g->bh * g->bw;
+  if (nb > UF_MAX_BLOCKS) return fail(UF_ERR_UNSUPPORTED, "%lld blocks per chunk, at most %d", (long long)nb, UF_MAX_BLOCKS);
+  if (tile > 255) return fail(UF_ERR_UNSUPPORTED, "blocks of %lld tokens, at most 255", (long long)tile);
+  if (nb * tile > INT32_MAX) return fail(UF_ERR_ARG, "block-order length too large");
+  if (padded) *padded = int32_t(nb * tile);
+  if (nblocks) *nblocks = int32_t(nb);
+  return UF_OK;
+}
+
+int check_local(const uf_kv* kv, int32_t local_r) {
+  if (local_r == 0) return UF_OK;
+  if (local_r < 0 || local_r % 2 == 0) return fail(UF_ERR_ARG, "local_r must be 0 or odd and positive (got %d)", local_r);
+  if (!kv->blocked) return fail(UF_ERR_ARG, "local_r needs block geometry (uf_kv_set_block_geom)");
+  return UF_OK;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -161,6 +201,7 @@ int write_chunk(uf_kv* kv, int32_t slot, const void* d_k, const void* d_v, void*
     a.NT = kv->nt;
     a.tail = kv->tail;
     a.pad = (kv->d.flags & UF_F_POISON_PAD) ? uint16_t(0x461C) : uint16_t(0);  // bf16 9984.0
+    a.tv = kv->tile_valid(0);
     hipError_t e = uf::launch_kv_append(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(UF_ERR_HIP, "kv_append launch: %s", hipGetErrorString(e));
   }
@@ -252,12 +293,15 @@ int uf_build_tile_lists(const uf_kv* kv, const uf_keep_rule* rule, void* d_lists
     return fail(UF_ERR_ARG, "p_prior must lie in [0, 1]");
   if ((rule->keep_sink != 0 && rule->keep_sink != 1) || (rule->keep_current != 0 && rule->keep_current != 1))
     return fail(UF_ERR_ARG, "keep_sink and keep_current must be 0 or 1");
+  if (rule->reserved != 0) return fail(UF_ERR_ARG, "reserved must be 0");
+  if (int s = check_local(kv, rule->local_r)) return s;
   if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
   const uf_lists_layout lay = kv->layout();
   if (kv->dry()) return ok();
   if (d_lists == nullptr || !aligned(d_lists, 256)) return fail(UF_ERR_ARG, "lists must be non-null and 256-byte aligned");
   if (bytes < lay.total_bytes) return fail(UF_ERR_ARG, "lists buffer has %zu bytes, needs %zu", bytes, lay.total_bytes);
   uf::ListArgs a{};
+  a.tv = kv->tile_valid(rule->local_r);
   a.lists = static_cast<uint8_t*>(d_lists);
   a.idx_offset = lay.idx_offset;
   a.mask_offset = lay.mask_offset;
@@ -287,7 +331,7 @@ int uf_build_topk_lists(const uf_kv* kv, const void* d_q, const uf_topk_rule* ru
   if (rule->budget < 0) return fail(UF_ERR_ARG, "budget must be >= 0 (got %d)", rule->budget);
   if ((rule->keep_sink != 0 && rule->keep_sink != 1) || (rule->keep_current != 0 && rule->keep_current != 1))
     return fail(UF_ERR_ARG, "keep_sink and keep_current must be 0 or 1");
-  if (rule->reserved != 0) return fail(UF_ERR_ARG, "reserved must be 0");
+  if (int s = check_local(kv, rule->local_r)) return s;
   if (kv->live.empty()) return fail(UF_ERR_EMPTY, "window holds no chunk");
   const int32_t nk = int32_t(kv->live.size()) * kv->nt;
   const int32_t lo = (kv->live.front().sink && rule->keep_sink) ? kv->nt : 0;
@@ -320,6 +364,7 @@ int uf_build_topk_lists(const uf_kv* kv, const void* d_q, const uf_topk_rule* ru
   a.cand_lo = lo;
   a.cand_hi = hi;
   a.budget = rule->budget;
+  a.tv = kv->tile_valid(rule->local_r);
   for (size_t p = 0; p < kv->live.size(); ++p) a.slot_of[p] = kv->live[p].slot;
   const size_t lds = std::max<size_t>(size_t(a.G) * size_t(nc) * 5, 16);
   hipError_t e = uf::launch_topk_lists(a, lds, static_cast<hipStream_t>(stream));
@@ -373,6 +418,7 @@ int attn_args(const uf_kv* kv, const void* d_q, const void* d_lists, float scale
   a.scale_log2 = scale * 1.4426950408889634f;
   a.split = 1;
   a.work = nullptr;
+  a.tv = kv->tile_valid(0);
   for (size_t p = 0; p < kv->live.size(); ++p) a.slot_of[p] = kv->live[p].slot;
   *out = a;
   return UF_OK;
@@ -419,6 +465,65 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
   a.work = static_cast<float*>(d_work);
   hipError_t e = uf::launch_attn_fwd_t128_pp_split(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_block_geom_tokens(const uf_block_geom* g, int32_t* padded_tokens, int32_t* n_blocks) {
+  if (int s = check_geom(g, padded_tokens, n_blocks)) return s;
+  return ok();
+}
+
+int uf_kv_set_block_geom(uf_kv* kv, const uf_block_geom* g) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  int32_t padded = 0, nb = 0;
+  if (int s = check_geom(g, &padded, &nb)) return s;
+  if (!kv->live.empty() || kv->next_seq != 0) return fail(UF_ERR_ARG, "block geometry must be set on a new, empty window");
+  if (g->bt * g->bh * g->bw != kv->d.tile)
+    return fail(UF_ERR_ARG, "block of %d tokens, tile is %d", g->bt * g->bh * g->bw, kv->d.tile);
+  if (padded != kv->d.chunk_tokens)
+    return fail(UF_ERR_ARG, "chunk_tokens must be the block-order length %d (got %d)", padded, kv->d.chunk_tokens);
+  kv->blocked = true;
+  kv->geom = *g;
+  kv->nbh = (g->grid_h + g->bh - 1) / g->bh;
+  kv->nbw = (g->grid_w + g->bw - 1) / g->bw;
+  for (int32_t j = 0; j < nb; ++j) {
+    const int32_t bti = j / (kv->nbh * kv->nbw), bhi = (j / kv->nbw) % kv->nbh, bwi = j % kv->nbw;
+    const int32_t n = std::min(g->bt, g->frames - bti * g->bt) * std::min(g->bh, g->grid_h - bhi * g->bh) *
+                      std::min(g->bw, g->grid_w - bwi * g->bw);
+    kv->block_valid[j] = uint8_t(n);
+  }
+  return ok();
+}
+
+int uf_block_permute(const uf_block_geom* g, int32_t batch, int32_t heads, int32_t head_dim, const void* d_src,
+                     void* d_dst, int32_t inverse, void* stream) {
+  int32_t padded = 0, nb = 0;
+  if (int s = check_geom(g, &padded, &nb)) return s;
+  if (batch < 1 || heads < 1) return fail(UF_ERR_ARG, "batch and heads must be >= 1");
+  if (head_dim != 128) return fail(UF_ERR_UNSUPPORTED, "head_dim must be 128 (got %d)", head_dim);
+  if (inverse != 0 && inverse != 1) return fail(UF_ERR_ARG, "inverse must be 0 or 1");
+  const int64_t tokens = int64_t(g->frames) * g->grid_h * g->grid_w;
+  if (int64_t(batch) * padded * heads > INT32_MAX) return fail(UF_ERR_ARG, "shape too large");
+  if (d_src == nullptr || d_dst == nullptr || !aligned(d_src, 16) || !aligned(d_dst, 16))
+    return fail(UF_ERR_ARG, "src and dst must be non-null and 16-byte aligned");
+  uf::PermuteArgs a{};
+  a.src = static_cast<const uint16_t*>(d_src);
+  a.dst = static_cast<uint16_t*>(d_dst);
+  a.B = batch;
+  a.H = heads;
+  a.frames = g->frames;
+  a.gh = g->grid_h;
+  a.gw = g->grid_w;
+  a.bt = g->bt;
+  a.bh = g->bh;
+  a.bw = g->bw;
+  a.nbh = (g->grid_h + g->bh - 1) / g->bh;
+  a.nbw = (g->grid_w + g->bw - 1) / g->bw;
+  a.tokens = int32_t(tokens);
+  a.padded = padded;
+  a.inverse = inverse;
+  hipError_t e = uf::launch_block_permute(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "block_permute launch: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -72,6 +72,10 @@ class KVWindow:
             _check_chunk(v, "v", self.B, self.L, self.H, self.D)
         L.uf_kv_replace_newest(self.handle, k, v, stream)
 
+    def set_block_geom(self, frames, grid_h, grid_w, bt=2, bh=8, bw=8):
+        """Tiles become (bt, bh, bw) blocks of a frames x grid_h x grid_w chunk (before any append)."""
+        L.uf_kv_set_block_geom(self.handle, L.uf_block_geom(frames, grid_h, grid_w, bt, bh, bw))
+
     def evict(self, n=1):
         L.uf_kv_evict(self.handle, n)
 
@@ -82,16 +86,17 @@ class KVWindow:
         return L.uf_kv_logical(self.handle, pos)
 
     # -- lists --------------------------------------------------------------
-    def build_lists(self, seed, p_prior, keep_sink=True, keep_current=True, stream=None):
-        rule = L.uf_keep_rule(seed & 0xFFFFFFFFFFFFFFFF, float(p_prior), int(keep_sink), int(keep_current))
+    def build_lists(self, seed, p_prior, keep_sink=True, keep_current=True, stream=None, local_r=0):
+        rule = L.uf_keep_rule(seed & 0xFFFFFFFFFFFFFFFF, float(p_prior), int(keep_sink), int(keep_current),
+                              int(local_r), 0)
         L.uf_build_tile_lists(self.handle, rule, self.lists, None, stream)
         return self.lists
 
-    def build_topk_lists(self, q, budget, keep_sink=True, keep_current=True, stream=None):
+    def build_topk_lists(self, q, budget, keep_sink=True, keep_current=True, stream=None, local_r=0):
         """Lists by content-adaptive top-k from the current chunk's queries q [B, L, H, D] bf16."""
         if not self.dry:
             _check_chunk(q, "q", self.B, self.L, self.H, self.D)
-        rule = L.uf_topk_rule(int(budget), int(keep_sink), int(keep_current), 0)
+        rule = L.uf_topk_rule(int(budget), int(keep_sink), int(keep_current), int(local_r))
         L.uf_build_topk_lists(self.handle, q, rule, self.lists, None, stream)
         return self.lists
 

@@ -1,0 +1,203 @@
+"""3-D block tiling on the GPU (block order of tokens, per-block valid rows,
+the local window M_local) against the CPU oracle.
+
+The GPU path permutes raster tokens into block order (uf_block_permute),
+runs the window with block geometry, and permutes the output back; the oracle
+evaluates the same attention directly in raster order over the tokens of the
+kept blocks, so the two share nothing but the definition.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_common import LSE_TOL, REL_TOL, f64, log, require_gpu, row_rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _permute(P, g, x, inverse):
+    B, _, H, D = x.shape
+    n = g.tokens if inverse else g.padded_tokens
+    out = torch.empty((B, n, H, D), dtype=x.dtype, device=x.device)
+    P.uf_block_permute(P.uf_block_geom(g.frames, g.grid_h, g.grid_w, g.bt, g.bh, g.bw), B, H, x, out, inverse)
+    return out
+
+
+@pytest.mark.parametrize("geom", [(3, 10, 12, 2, 4, 8), (3, 68, 120, 2, 8, 8), (1, 9, 17, 1, 8, 8)])
+def test_block_permute_matches_oracle_order(geom):
+    P = require_gpu()
+    g = oracle.BlockGeom(*geom)
+    x = synth.custom_tensor((2, g.tokens, 3, 128), 31, 0, "k").cuda()
+    y = _permute(P, g, x, 0)
+    torch.cuda.synchronize()
+    src = torch.from_numpy(oracle.block_order(g)).cuda()
+    want = torch.zeros_like(y)
+    valid = src >= 0
+    want[:, valid] = x[:, src[valid]]
+    assert torch.equal(y, want)
+    back = _permute(P, g, y, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(back, x)
+
+
+class BlockCase:
+    """A blocked window on the GPU and the same chunks, in raster order, for the oracle."""
+
+    def __init__(self, P, g, B, H, max_chunks, pin_sink, seed):
+        self.P, self.g, self.B, self.H, self.seed = P, g, B, H, seed
+        self.win = P.KVWindow(B, H, g.padded_tokens, g.tile, max_chunks, pin_sink)
+        self.win.set_block_geom(g.frames, g.grid_h, g.grid_w, g.bt, g.bh, g.bw)
+        self.ring = oracle.RingModel(max_chunks, pin_sink)
+        self.n = 0
+
+    def draw(self, chunk, name):
+        return synth.custom_tensor((self.B, self.g.tokens, self.H, 128), self.seed, chunk, name, device="cuda")
+
+    def append(self):
+        if self.win.info().n_live == self.win.desc.max_chunks:
+            self.win.evict(1)
+            self.ring.evict(1)
+        k, v = self.draw(self.n, "k"), self.draw(self.n, "v")
+        self.win.append(_permute(self.P, self.g, k, 0), _permute(self.P, self.g, v, 0))
+        self.ring.append(f64(k), f64(v))
+        self.n += 1
+
+    def meta_ring(self):
+        meta = oracle.RingModel(self.ring.max_chunks, self.ring.pin_sink)
+        z = np.broadcast_to(np.zeros(1), (self.B, self.g.padded_tokens, self.H, 1))
+        meta.live = [oracle.ring.Chunk(c.seq, c.sink, z, None) for c in self.ring.live]
+        return meta
+
+    def local_bits(self, r):
+        nb = self.g.n_blocks
+        return np.tile(oracle.local_mask(self.g, r), (1, self.ring.n_live)) if r else np.ones((nb, nb * self.ring.n_live), bool)
+
+    def oracle_bernoulli(self, p, r):
+        bits = oracle.keep_bits(self.meta_ring(), self.g.tile, oracle.KeepRule(self.seed, p))
+        return bits & self.local_bits(r)[None, None]
+
+    def oracle_topk(self, q, budget, r):
+        chunks = self.ring.logical_chunks()
+        cur = self.ring.current
+        nb = self.g.n_blocks
+        forced = np.zeros(nb * len(chunks), bool)
+        for pos, c in enumerate(chunks):
+            if c.sink or c.seq == cur.seq:
+                forced[pos * nb:(pos + 1) * nb] = True
+        qh = f64(q)
+        bits = np.zeros((self.B, self.H, nb, nb * len(chunks)), bool)
+        for b in range(self.B):
+            for h in range(self.H):
+                qm = oracle.block_means(qh[b, :, h], self.g)
+                km = np.concatenate([oracle.block_means(c.k[b, :, h], self.g) for c in chunks])
+                s = oracle.block_scores(qm, km)
+                for i in range(nb):
+                    bits[b, h, i] = forced | oracle.select_topk(s[i], ~forced, budget)
+        return bits & self.local_bits(r)[None, None]
+
+    def gpu_lists(self):
+        torch.cuda.synchronize()
+        c, i, m = self.win.lists_views()
+        return c.cpu().numpy(), i.cpu().numpy(), m.cpu().numpy().view(np.uint32)
+
+    def compare_lists(self, bits):
+        want = oracle.lists_from_bits(bits, self.win.info().nk_cap)
+        for got, exp in zip(self.gpu_lists(), want):
+            assert np.array_equal(got, exp)
+
+    def attention(self, q, blocks=None):
+        """GPU O and LSE in raster order; (optional) only the query blocks listed are checked."""
+        o, lse = self.win.attention(_permute(self.P, self.g, q, 0))
+        o_r = _permute(self.P, self.g, o, 1)
+        torch.cuda.synchronize()
+        src = oracle.block_order(self.g)
+        lse_r = np.empty((self.B, self.H, self.g.tokens))
+        lb = lse.cpu().numpy()
+        lse_r[:, :, src[src >= 0]] = lb[:, :, np.nonzero(src >= 0)[0]]
+        return f64(o_r), lse_r
+
+    def check_attention(self, q, bits, heads=None, blocks=None):
+        o, lse = self.attention(q)
+        qh = f64(q)
+        blk = oracle.block_of_token(self.g)
+        worst, lworst = 0.0, 0.0
+        for b in range(self.B):
+            for h in (range(self.H) if heads is None else heads):
+                ks = [c.k[b, :, h] for c in self.ring.logical_chunks()]
+                vs = [c.v[b, :, h] for c in self.ring.logical_chunks()]
+                bb = bits[b, h].copy()
+                if blocks is not None:
+                    keep_rows = np.zeros(self.g.n_blocks, bool)
+                    keep_rows[list(blocks)] = True
+                    bb[~keep_rows] = False
+                O, LSE = oracle.attention_in_raster(ks, vs, qh[b, :, h], self.g, bb, 1 / math.sqrt(128))
+                rows = np.nonzero(np.isin(blk, list(blocks)))[0] if blocks is not None else np.arange(self.g.tokens)
+                worst = max(worst, row_rel_err(o[b, rows, h], O[rows]))
+                lworst = max(lworst, float(np.abs(lse[b, h, rows] - LSE[rows]).max()))
+        log(f"  rel_err={worst:.3e} lse_err={lworst:.3e}")
+        assert worst <= REL_TOL and lworst <= LSE_TOL
+
+
+SMALL = oracle.BlockGeom(3, 10, 12, 2, 4, 8)     # 12 blocks of 64, edge blocks partial
+
+
+@pytest.mark.parametrize("r", [0, 1, 3])
+def test_blocked_bernoulli_lists_and_attention(r):
+    P = require_gpu()
+    log(f"blocks bernoulli r={r}")
+    case = BlockCase(P, SMALL, 2, 3, 4, True, seed=41)
+    for _ in range(5):
+        case.append()
+    case.win.build_lists(case.seed, 0.5, local_r=r)
+    bits = case.oracle_bernoulli(0.5, r)
+    case.compare_lists(bits)
+    case.check_attention(case.draw(99, "q"), bits)
+
+
+@pytest.mark.parametrize("r", [0, 3])
+def test_blocked_topk_lists_and_attention(r):
+    P = require_gpu()
+    log(f"blocks topk r={r}")
+    case = BlockCase(P, SMALL, 1, 2, 4, True, seed=43)
+    for _ in range(4):
+        case.append()
+    q = case.draw(98, "q")
+    case.win.build_topk_lists(_permute(P, SMALL, q, 0), 5, local_r=r)
+    bits = case.oracle_topk(q, 5, r)
+    case.compare_lists(bits)
+    case.check_attention(q, bits)
+
+
+def test_blocked_pooled_keys_follow_block_counts():
+    P = require_gpu()
+    case = BlockCase(P, SMALL, 1, 2, 3, False, seed=45)
+    for _ in range(2):
+        case.append()
+    torch.cuda.synchronize()
+    km = case.win.kmean_view().cpu().numpy()
+    for pos, c in enumerate(case.ring.logical_chunks()):
+        slot, _ = case.win.logical(pos)
+        for h in range(2):
+            assert np.array_equal(km[slot, 0, h], oracle.block_means(c.k[0, :, h], SMALL))
+
+
+def test_paper_geometry_1k_local_window():
+    """The paper's (2, 8, 8) blocks on the 1K grid (3 x 68 x 120, 270 blocks with
+    partial edge blocks), r = 9: lists bit for bit on every head, attention on
+    sampled query blocks of two heads."""
+    P = require_gpu()
+    g = oracle.BlockGeom(3, 68, 120, 2, 8, 8)
+    log("blocks 1k geometry r=9")
+    case = BlockCase(P, g, 1, 4, 5, True, seed=47)
+    for _ in range(5):
+        case.append()
+    case.win.build_lists(case.seed, 0.25, local_r=9)
+    bits = case.oracle_bernoulli(0.25, 9)
+    case.compare_lists(bits)
+    q = case.draw(97, "q")
+    case.check_attention(q, bits, heads=[0, 3], blocks=[0, 14, 134, 269])
