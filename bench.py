@@ -180,6 +180,91 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     return res, state
 
 
+def run_blocked(P, wl, steps, warmup, local_r=9, block=(2, 8, 8), n_src=3):
+    """The workload on 3-D blocks (the paper's (2, 8, 8) tiling, Sec. 2.3.1 (a)) with the
+    local window M_local(r): per step, permute the chunk's K, V and Q from raster to
+    block order, append, build Bernoulli lists intersected with M_local, attend, and
+    permute O back to raster order."""
+    import numpy as np
+    import torch
+    import synth
+
+    dev = torch.device("cuda", 0)
+    B, H = wl.batch, wl.heads
+    geom = P.uf_block_geom(wl.frames, wl.grid_h, wl.grid_w, *block)
+    padded, nb = P.uf_block_geom_tokens(geom)
+    T = block[0] * block[1] * block[2]
+    win = P.KVWindow(B, H, padded, T, wl.max_chunks, wl.pin_sink, device=dev)
+    win.set_block_geom(wl.frames, wl.grid_h, wl.grid_w, *block)
+    srcs = [{name: synth.chunk_tensor(wl, c, name, device="cuda") for name in ("k", "v", "q")}
+            for c in range(n_src)]
+    blk = {name: torch.empty((B, padded, H, D), dtype=torch.bfloat16, device=dev) for name in ("k", "v", "q", "o")}
+    o_raster = torch.empty_like(srcs[0]["q"])
+    lse = torch.empty((B, H, padded), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def permute(x, y, inverse):
+        P.uf_block_permute(geom, B, H, x, y, inverse)
+
+    for c in range(wl.window_chunks - 1):
+        permute(srcs[c % n_src]["k"], blk["k"], 0)
+        permute(srcs[c % n_src]["v"], blk["v"], 0)
+        win.append(blk["k"], blk["v"])
+    total = warmup + steps
+    lists = [torch.empty(win.layout.total_bytes, dtype=torch.uint8, device=dev) for _ in range(total)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(total)]
+
+    def step(s):
+        src = srcs[(wl.window_chunks - 1 + s) % n_src]
+        if win.info().n_live == wl.max_chunks:
+            win.evict(1)
+        e = ev[s]
+        e[0].record(stream)
+        permute(src["k"], blk["k"], 0)
+        permute(src["v"], blk["v"], 0)
+        permute(src["q"], blk["q"], 0)
+        e[1].record(stream)
+        win.append(blk["k"], blk["v"])
+        e[2].record(stream)
+        win.lists = lists[s]
+        win.build_lists(wl.seed, wl.p_prior, local_r=local_r)
+        e[3].record(stream)
+        win.attention(blk["q"], out=blk["o"], lse=lse)
+        e[4].record(stream)
+        permute(blk["o"], o_raster, 1)
+        e[5].record(stream)
+
+    for s in range(warmup):
+        step(s)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(warmup, total):
+        step(s)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    span = lambda a, b: sum(ev[s][a].elapsed_time(ev[s][b]) for s in range(warmup, total)) / steps
+    counts = np.zeros(nb, dtype=np.int64)
+    for j in range(nb):   # valid tokens of block j (raster grid)
+        nbh, nbw = -(-wl.grid_h // block[1]), -(-wl.grid_w // block[2])
+        bti, bhi, bwi = j // (nbh * nbw), (j // nbw) % nbh, j % nbw
+        counts[j] = (min(block[0], wl.frames - bti * block[0]) * min(block[1], wl.grid_h - bhi * block[1]) *
+                     min(block[2], wl.grid_w - bwi * block[2]))
+    cnt = torch.from_numpy(counts).to(dev)
+    kept = 0
+    for s in range(warmup, total):
+        _, idx, _ = win.lists_views(lists[s])
+        vk = torch.where(idx >= 0, cnt[idx.clamp(min=0) % nb], torch.zeros_like(idx, dtype=torch.int64)).sum(-1)
+        kept += int((vk * cnt[None, None, :]).sum().item()) * 4 * D
+    kept /= steps
+    attn_ms = span(3, 4)
+    dense = 4 * D * B * H * wl.chunk_tokens * (wl.chunk_tokens * wl.window_chunks)
+    return {"workload": f"{wl.name} on ({block[0]}, {block[1]}, {block[2]}) blocks, local window r = {local_r}",
+            "blocks_per_chunk": nb, "ms_per_step": ms_step, "attn_ms": attn_ms,
+            "attn_tflops": kept / (attn_ms * 1e-3) / 1e12, "kept_fraction": kept / dense,
+            "permute_in_us": span(0, 1) * 1e3, "append_us": span(1, 2) * 1e3, "lists_us": span(2, 3) * 1e3,
+            "permute_out_us": span(4, 5) * 1e3}
+
+
 def sparsity_sweep(wl, state, sparsities=(0.12, 0.35, 0.58, 0.72, 0.82), reps=10):
     """Attention time against sparsity on the final window of a run (the shape of the
     paper's sparsity-ratio ablation, App. L): pure top-k lists over the whole window
@@ -287,6 +372,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--split", type=int, default=0,
                     help="split-KV attention with this many list slices per row (0: whole rows)")
+    ap.add_argument("--blocks", action="store_true",
+                    help="also run the workload on (2, 8, 8) blocks with the local window r = 9")
     ap.add_argument("--sweep", action="store_true",
                     help="also time the attention against sparsity (top-k lists, no forced chunks)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -348,6 +435,8 @@ def main():
     }
     if args.sweep:
         line["sweep"] = sparsity_sweep(wl, state)
+    if args.blocks:
+        line["blocks"] = run_blocked(P, wl, max(5, args.steps // 2), args.warmup)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, state, args.cpu_seconds)
     del state

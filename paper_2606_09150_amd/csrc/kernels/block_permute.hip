@@ -3,8 +3,9 @@
 // The (t, h, w) token grid of a chunk is divided into (bt, bh, bw) blocks
 // (Sec. 2.3.1 (a)); in block order every block owns one tile of bt*bh*bw rows
 // holding its valid tokens in raster (t, h, w) order, then padding rows.  One
-// workgroup per (b, block) copies the block's rows, H*128 bf16 each (16-byte
-// chunks): forward writes zero padding rows, inverse drops them.  HBM-bound.
+// workgroup per (b, block, head) copies the block's rows of that head, 128
+// bf16 each (16-byte chunks): forward writes zero padding rows, inverse drops
+// them.  HBM-bound.
 #include "../launch.h"
 
 namespace uf {
@@ -15,8 +16,9 @@ constexpr int kRowChunks = 16;   // 16-byte chunks per (token, head) row of 128 
 
 __global__ __launch_bounds__(kThreads) void block_permute_kernel(PermuteArgs a) {
   const int nb = (a.frames + a.bt - 1) / a.bt * a.nbh * a.nbw;
-  const int blk = blockIdx.x % nb;
-  const int b = blockIdx.x / nb;
+  const int head = blockIdx.x % a.H;
+  const int blk = (blockIdx.x / a.H) % nb;
+  const int b = blockIdx.x / a.H / nb;
   const int bti = blk / (a.nbh * a.nbw);
   const int bhi = (blk / a.nbw) % a.nbh;
   const int bwi = blk % a.nbw;
@@ -28,9 +30,9 @@ __global__ __launch_bounds__(kThreads) void block_permute_kernel(PermuteArgs a) 
   const int per_row = a.H * kRowChunks;
   const uint4* src = reinterpret_cast<const uint4*>(a.src);
   uint4* dst = reinterpret_cast<uint4*>(a.dst);
-  for (int c = threadIdx.x; c < tile * per_row; c += kThreads) {
-    const int r = c / per_row;
-    const int cc = c - r * per_row;
+  for (int c = threadIdx.x; c < tile * kRowChunks; c += kThreads) {
+    const int r = c / kRowChunks;
+    const int cc = head * kRowChunks + (c - r * kRowChunks);
     const size_t brow = size_t(b) * a.padded + size_t(blk) * tile + r;   // block-order row
     if (r < valid) {
       const int dt = r / (nh * nw);
@@ -52,7 +54,7 @@ __global__ __launch_bounds__(kThreads) void block_permute_kernel(PermuteArgs a) 
 
 hipError_t launch_block_permute(const PermuteArgs& a, hipStream_t stream) {
   const unsigned nb = unsigned((a.frames + a.bt - 1) / a.bt * a.nbh * a.nbw);
-  block_permute_kernel<<<unsigned(a.B) * nb, kThreads, 0, stream>>>(a);
+  block_permute_kernel<<<unsigned(a.B) * nb * unsigned(a.H), kThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 
