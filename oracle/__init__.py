@@ -25,6 +25,8 @@ It is a plain, slow, obviously correct restatement of what the method computes
 * ``blocks``    -- the 3-D (b_t, b_h, b_w) block tiling of a chunk's token
                    grid, the block order of tokens, the r x r local window
                    mask M_local, and attention evaluated in raster order.
+* ``backward``  -- gradients dq, dk, dv of the masked attention (the training
+                   side of the same forward), float64.
 * ``attention`` -- softmax attention of the current chunk's queries over the
                    union of kept key tiles (Eq. 4 mask semantics), computed as
                    masked dense attention in float64.
@@ -60,6 +62,7 @@ from .blocks import (
     local_mask,
     attention_in_raster,
 )
+from .backward import sparse_causal_attention_bwd
 from .attention import (
     sparse_causal_attention,
     sparse_causal_attention_rows,
@@ -90,6 +93,7 @@ __all__ = [
     "select_topk",
     "topk_scores",
     "topk_bits",
+    "sparse_causal_attention_bwd",
     "sparse_causal_attention",
     "sparse_causal_attention_rows",
     "dense_keys",

@@ -1,0 +1,71 @@
+"""Oracle of the block-sparse chunk-causal attention backward (test infrastructure only).
+
+The student of Phase I is trained through sparse causal attention (Sec. 2.3.1:
+the same Eq. 4 mask in the generator that DMD updates), so the training side
+needs the gradients of the forward defined in ``attention``: for one head and
+query row r with kept key set C(r),
+
+    p_rc  = exp(s_rc - lse_r),  s_rc = scale * <q_r, k_c>     (c in C(r))
+    o_r   = sum_c p_rc v_c
+
+and an upstream gradient do_r, the chain rule gives
+
+    dv_c  = sum_{r: c in C(r)} p_rc do_r
+    dp_rc = <do_r, v_c>
+    delta_r = sum_c p_rc dp_rc = <do_r, o_r>
+    ds_rc = p_rc (dp_rc - delta_r)
+    dq_r  = scale * sum_c ds_rc k_c
+    dk_c  = scale * sum_{r: c in C(r)} ds_rc q_r
+
+Keys outside every kept set get zero gradients; padding never exists here
+(chunks hold exactly their tokens).  Evaluated in float64 as masked dense
+products over the window's keys in logical order.
+"""
+
+import numpy as np
+
+from .attention import dense_keys, _kept_columns
+from .keep import tile_geometry
+
+
+def sparse_causal_attention_bwd(ring, q, do, bits, T: int, scale: float, heads=None):
+    """Gradients of the forward oracle.
+
+    q, do: [B, L, H, D] (current chunk queries and upstream gradient of O);
+    bits: [B, H, NQ, NK] keep set.  Returns (dq [B, L, H, D],
+    dk, dv [n_live, B, L, H, D] in logical chunk order), float64.
+    """
+    chunks = ring.logical_chunks()
+    B, L, H, D = q.shape
+    n_live = len(chunks)
+    nt, _ = tile_geometry(L, T)
+    sk = L * n_live
+    dq = np.zeros((B, L, H, D))
+    dk = np.zeros((n_live, B, L, H, D))
+    dv = np.zeros((n_live, B, L, H, D))
+    for b in range(B):
+        for h in (range(H) if heads is None else heads):
+            K, V = dense_keys(ring, b, h)
+            dK = np.zeros((sk, D))
+            dV = np.zeros((sk, D))
+            for i in range(nt):
+                r0, r1 = i * T, min((i + 1) * T, L)
+                cols = _kept_columns(np.nonzero(bits[b, h, i])[0], L, T, nt, sk)
+                if not cols.any():
+                    continue
+                Q = q[b, r0:r1, h].astype(np.float64)
+                dO = do[b, r0:r1, h].astype(np.float64)
+                Kc, Vc = K[cols], V[cols]
+                S = (Q @ Kc.T) * scale
+                P = np.exp(S - S.max(axis=1, keepdims=True))
+                P /= P.sum(axis=1, keepdims=True)
+                O = P @ Vc
+                dP = dO @ Vc.T
+                delta = (dO * O).sum(axis=1, keepdims=True)
+                dS = P * (dP - delta)
+                dq[b, r0:r1, h] = scale * (dS @ Kc)
+                dK[cols] += scale * (dS.T @ Q)
+                dV[cols] += P.T @ dO
+            dk[:, b, :, h] = dK.reshape(n_live, L, D)
+            dv[:, b, :, h] = dV.reshape(n_live, L, D)
+    return dq, dk, dv

@@ -1,0 +1,106 @@
+"""Pins of the backward oracle: central finite differences of the forward
+oracle, autograd of an independently written masked softmax attention in
+float64, and closed-form special cases."""
+
+import numpy as np
+import torch
+
+import oracle
+
+
+def _ring(B, L, H, D, n, pin, seed):
+    rng = np.random.default_rng(seed)
+    ring = oracle.RingModel(n, pin)
+    for _ in range(n):
+        ring.append(rng.standard_normal((B, L, H, D)), rng.standard_normal((B, L, H, D)))
+    q = rng.standard_normal((B, L, H, D))
+    do = rng.standard_normal((B, L, H, D))
+    return ring, q, do, rng
+
+
+def _bits(rng, B, H, nt, nk):
+    bits = rng.random((B, H, nt, nk)) < 0.6
+    bits[..., -1] = True          # every row keeps at least one tile
+    return bits
+
+
+def test_backward_matches_central_differences():
+    B, L, H, D, T = 1, 5, 1, 4, 2
+    ring, q, do, rng = _ring(B, L, H, D, 3, True, 1)
+    nt = 3
+    bits = _bits(rng, B, H, nt, 3 * nt)
+    scale = 0.7
+    dq, dk, dv = oracle.sparse_causal_attention_bwd(ring, q, do, bits, T, scale)
+
+    def f():
+        O, _ = oracle.sparse_causal_attention(ring, q, bits, T, scale)
+        return float((O * do).sum())
+
+    eps = 1e-6
+    for arr, grad in [(q, dq)] + [(c.k, dk[p]) for p, c in enumerate(ring.logical_chunks())] + \
+                     [(c.v, dv[p]) for p, c in enumerate(ring.logical_chunks())]:
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            keep = arr[idx]
+            arr[idx] = keep + eps
+            fp = f()
+            arr[idx] = keep - eps
+            fm = f()
+            arr[idx] = keep
+            num[idx] = (fp - fm) / (2 * eps)
+        assert np.allclose(grad, num, atol=1e-7, rtol=1e-6)
+
+
+def test_backward_matches_autograd_of_masked_attention():
+    B, L, H, D, T = 2, 7, 2, 8, 3
+    ring, q, do, rng = _ring(B, L, H, D, 4, False, 2)
+    nt = 3
+    bits = _bits(rng, B, H, nt, 4 * nt)
+    scale = 0.35
+    dq, dk, dv = oracle.sparse_causal_attention_bwd(ring, q, do, bits, T, scale)
+    chunks = ring.logical_chunks()
+    for b in range(B):
+        for h in range(H):
+            Q = torch.tensor(q[b, :, h], requires_grad=True)
+            Ks = [torch.tensor(c.k[b, :, h], requires_grad=True) for c in chunks]
+            Vs = [torch.tensor(c.v[b, :, h], requires_grad=True) for c in chunks]
+            K, V = torch.cat(Ks), torch.cat(Vs)
+            # token-level mask from the tile bits: query token r in tile r // T,
+            # key token (pos, t) in logical tile pos * nt + t // T
+            key_tile = torch.tensor([p * nt + t // T for p in range(len(chunks)) for t in range(L)])
+            qt = torch.arange(L) // T
+            mask = torch.tensor(bits[b, h])[qt][:, key_tile]
+            S = (Q @ K.T) * scale
+            S = S.masked_fill(~mask, float("-inf"))
+            O = torch.softmax(S, dim=1) @ V
+            (O * torch.tensor(do[b, :, h])).sum().backward()
+            assert np.allclose(Q.grad.numpy(), dq[b, :, h], atol=1e-10)
+            for p in range(len(chunks)):
+                assert np.allclose(Ks[p].grad.numpy(), dk[p, b, :, h], atol=1e-10)
+                assert np.allclose(Vs[p].grad.numpy(), dv[p, b, :, h], atol=1e-10)
+
+
+def test_backward_closed_forms():
+    B, L, H, D, T = 1, 6, 1, 4, 2
+    ring, q, do, rng = _ring(B, L, H, D, 2, False, 3)
+    bits = _bits(rng, B, H, 3, 6)
+    # equal values: dp = delta for every key, so ds = 0 and dq = dk = 0
+    v0 = ring.live[0].v[:, :1].copy()
+    for c in ring.live:
+        c.v = np.broadcast_to(v0, c.v.shape).copy()
+    dq, dk, dv = oracle.sparse_causal_attention_bwd(ring, q, do, bits, T, 0.5)
+    assert np.allclose(dq, 0, atol=1e-12) and np.allclose(dk, 0, atol=1e-12)
+    # shifting every key by one vector leaves dq unchanged (rows of ds sum to 0)
+    ring2, q2, do2, rng2 = _ring(B, L, H, D, 2, False, 4)
+    bits2 = _bits(rng2, B, H, 3, 6)
+    dq1, _, _ = oracle.sparse_causal_attention_bwd(ring2, q2, do2, bits2, T, 0.5)
+    shift = rng2.standard_normal(D)
+    for c in ring2.live:
+        c.k = c.k + shift
+    dq2, _, _ = oracle.sparse_causal_attention_bwd(ring2, q2, do2, bits2, T, 0.5)
+    assert not np.allclose(dq1, 0) and np.allclose(dq1, dq2, atol=1e-10)
+    # keys no row keeps get zero gradients
+    bits3 = np.zeros((1, 1, 3, 6), bool)
+    bits3[..., 4] = True
+    _, dk3, dv3 = oracle.sparse_causal_attention_bwd(ring2, q2, do2, bits3, T, 0.5)
+    assert np.all(dk3[0] == 0) and np.all(dv3[0] == 0) and np.any(dv3[1] != 0)
