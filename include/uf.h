@@ -18,6 +18,7 @@
  *                               (seeded Bernoulli stand-in), or
  *   uf_build_topk_lists         the same lists by content-adaptive top-k (Eq. 4)
  *   uf_sparse_causal_attn_fwd   attention of the current chunk's queries
+ *   uf_sparse_causal_attn_bwd   its gradients (dQ, dK, dV)
  *
  * Conventions
  *   - bf16 tensors are raw IEEE bfloat16 bit patterns (uint16).
@@ -299,6 +300,27 @@ int uf_attn_split_work_bytes(const uf_kv* kv, int32_t n_split, size_t* bytes);
 int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
                                     void* d_o, float* d_lse, int32_t n_split, void* d_work,
                                     size_t work_bytes, void* stream);
+
+/* Backward of uf_sparse_causal_attn_fwd (the student's training side of
+ * Sec. 2.3.1: gradients through the same Eq. 4 mask).  With p = exp(scale*q.k
+ * - LSE) over the kept keys of each row, delta = <dO, O> per row and
+ * dS = p * (dO.v - delta):
+ *   dQ = scale * sum_c dS_c k_c,  dK_c = scale * sum_r dS_rc q_r,
+ *   dV_c = sum_r p_rc dO_r
+ * (keys of no kept tile and padding rows get zero).  d_q, d_o (the forward's
+ * output), d_do: [B, L, H, D] bf16, 16-byte aligned; d_lse [B, H, L] fp32, the
+ * forward's LSE for the same window, queries and d_lists (both the index and
+ * the mask sections are read, so they must come from one list build).
+ * Outputs, fp32, 16-byte aligned, fully overwritten: d_dq [B, L, H, D];
+ * d_dk, d_dv [n_live, B, L, H, D] in logical chunk order (position 0 first).
+ * d_work (16-byte aligned, >= uf_attn_bwd_work_bytes) is caller-owned scratch,
+ * overwritten.  Deterministic (no atomics).  Needs 128-token tiles and
+ * head_dim 128.  Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED (tile 64),
+ * UF_ERR_EMPTY, UF_ERR_HIP. */
+int uf_attn_bwd_work_bytes(const uf_kv* kv, size_t* bytes);
+int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
+                              const float* d_lse, const void* d_lists, float scale, float* d_dq,
+                              float* d_dk, float* d_dv, void* d_work, size_t work_bytes, void* stream);
 
 /* Static text of a status code. */
 const char* uf_status_string(int status);

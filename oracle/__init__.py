@@ -62,7 +62,7 @@ from .blocks import (
     local_mask,
     attention_in_raster,
 )
-from .backward import sparse_causal_attention_bwd
+from .backward import sparse_causal_attention_bwd, sparse_causal_attention_bwd_rows
 from .attention import (
     sparse_causal_attention,
     sparse_causal_attention_rows,
@@ -94,6 +94,7 @@ __all__ = [
     "topk_scores",
     "topk_bits",
     "sparse_causal_attention_bwd",
+    "sparse_causal_attention_bwd_rows",
     "sparse_causal_attention",
     "sparse_causal_attention_rows",
     "dense_keys",

@@ -69,3 +69,33 @@ def sparse_causal_attention_bwd(ring, q, do, bits, T: int, scale: float, heads=N
             dk[:, b, :, h] = dK.reshape(n_live, L, D)
             dv[:, b, :, h] = dV.reshape(n_live, L, D)
     return dq, dk, dv
+
+
+def sparse_causal_attention_bwd_rows(ring, q, do, bits, T: int, scale: float, samples):
+    """dq of the same definition at sampled (b, h, r) query rows only: each row
+    needs just its own kept keys (its softmax, o_r and delta_r).  Returns
+    dq [n, D] float64."""
+    q = np.asarray(q, np.float64)
+    do = np.asarray(do, np.float64)
+    B, L, H, D = q.shape
+    nt, _ = tile_geometry(L, T)
+    sk = ring.n_live * L
+    samples = list(samples)
+    out = np.zeros((len(samples), D))
+    cache = {}
+    for n, (b, h, r) in enumerate(samples):
+        if (b, h) not in cache:
+            cache = {(b, h): dense_keys(ring, b, h)}
+        K, V = cache[(b, h)]
+        cols = _kept_columns(np.nonzero(bits[b, h, r // T])[0], L, T, nt, sk)
+        if not cols.any():
+            continue
+        Kc, Vc = K[cols], V[cols]
+        s = (Kc @ q[b, r, h]) * scale
+        p = np.exp(s - s.max())
+        p /= p.sum()
+        o = p @ Vc
+        dp = Vc @ do[b, r, h]
+        ds = p * (dp - do[b, r, h] @ o)
+        out[n] = scale * (ds @ Kc)
+    return out

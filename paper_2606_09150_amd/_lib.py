@@ -90,6 +90,9 @@ _SIGNATURES = {
     "uf_attn_split_work_bytes": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]),
     "uf_sparse_causal_attn_fwd_split": (ctypes.c_int, [_P, _P, _P, ctypes.c_float, _P, _P, ctypes.c_int32, _P,
                                                        ctypes.c_size_t, _P]),
+    "uf_attn_bwd_work_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
+    "uf_sparse_causal_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P,
+                                                 ctypes.c_size_t, _P]),
     "uf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "uf_last_error": (ctypes.c_char_p, []),
 }
@@ -252,6 +255,20 @@ def uf_sparse_causal_attn_fwd_split(handle, q, lists, scale: float, o, lse, n_sp
     s = None if q is None else _stream_ptr(stream)
     _check(load().uf_sparse_causal_attn_fwd_split(handle, _ptr(q), _ptr(lists), ctypes.c_float(scale), _ptr(o),
                                                   _ptr(lse), n_split, _ptr(work), n, s))
+
+
+def uf_attn_bwd_work_bytes(handle) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().uf_attn_bwd_work_bytes(handle, ctypes.byref(out)))
+    return out.value
+
+
+def uf_sparse_causal_attn_bwd(handle, q, o, do, lse, lists, scale: float, dq, dk, dv, work,
+                              work_bytes: int = None, stream=None) -> None:
+    n = work_bytes if work_bytes is not None else (0 if work is None else work.numel() * work.element_size())
+    s = None if q is None else _stream_ptr(stream)
+    _check(load().uf_sparse_causal_attn_bwd(handle, _ptr(q), _ptr(o), _ptr(do), _ptr(lse), _ptr(lists),
+                                            ctypes.c_float(scale), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(work), n, s))
 
 
 def uf_status_string(status: int) -> str:

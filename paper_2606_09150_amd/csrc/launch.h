@@ -97,6 +97,33 @@ struct AttnArgs {
   TileValid tv;
 };
 
+// Backward of the attention.  The workspace holds, per query tile (b, h, i),
+// Q and dO row-major and transposed (the query index of the transposed tiles
+// in swap23 order within groups of 16), then LSE*log2(e) and delta = <dO, O>
+// per query; and, per window key tile (logical position, b, h, t), K^T (keys
+// in swap23 order) and V row-major.
+constexpr size_t kBwdQTile = 4 * 32768 + 1024;
+constexpr size_t kBwdKTile = 2 * 32768;
+struct BwdArgs {
+  const uint16_t* q;      // [B, L, H, D]
+  const uint16_t* o;      // [B, L, H, D]
+  const uint16_t* dout;   // [B, L, H, D]
+  const float* lse;       // [B, H, L]
+  const uint8_t* pool;
+  const int32_t* counts;  // lists
+  const int32_t* idx;
+  const uint32_t* mask;
+  float* dq;              // [B, L, H, D]
+  float* dk;              // [n_live][B, L, H, D]
+  float* dv;              // [n_live][B, L, H, D]
+  uint8_t* work;
+  int32_t B, H, L, T, NT, tail, nk, nk_cap, mask_words, n_live;
+  float scale, scale_log2;
+  int32_t slot_of[UF_MAX_CHUNKS];
+  TileValid tv;
+};
+hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream);
+
 // Block-order permutation of [B, tokens, H, 128] bf16 rows.
 struct PermuteArgs {
   const uint16_t* src;

@@ -468,6 +468,74 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
   return ok();
 }
 
+namespace {
+
+// Query-tile records for every row, then key-tile records for every window
+// position the handle can hold, so the size does not change as chunks come
+// and go.
+size_t bwd_work_bytes(const uf_kv* kv) {
+  const size_t rows = size_t(kv->layout().rows);
+  return rows * uf::kBwdQTile + size_t(kv->d.max_chunks) * rows * uf::kBwdKTile;
+}
+
+}  // namespace
+
+int uf_attn_bwd_work_bytes(const uf_kv* kv, size_t* bytes) {
+  if (kv == nullptr || bytes == nullptr) return fail(UF_ERR_ARG, "null argument");
+  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "the backward needs 128-token tiles");
+  *bytes = bwd_work_bytes(kv);
+  return ok();
+}
+
+int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
+                              const float* d_lse, const void* d_lists, float scale, float* d_dq, float* d_dk,
+                              float* d_dv, void* d_work, size_t work_bytes, void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "the backward needs 128-token tiles");
+  uf::AttnArgs f{};
+  if (int s = attn_args(kv, d_q, d_lists, scale, const_cast<void*>(d_o), const_cast<float*>(d_lse), &f)) return s;
+  if (kv->dry()) return ok();
+  if (d_do == nullptr || d_lse == nullptr || d_dq == nullptr || d_dk == nullptr || d_dv == nullptr)
+    return fail(UF_ERR_ARG, "do, lse, dq, dk or dv is null");
+  if (!aligned(d_do, 16) || !aligned(d_dq, 16) || !aligned(d_dk, 16) || !aligned(d_dv, 16))
+    return fail(UF_ERR_ARG, "do, dq, dk and dv must be 16-byte aligned");
+  if (d_work == nullptr || !aligned(d_work, 16)) return fail(UF_ERR_ARG, "work must be non-null and 16-byte aligned");
+  if (work_bytes < bwd_work_bytes(kv))
+    return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, bwd_work_bytes(kv));
+  const uf_lists_layout lay = kv->layout();
+  if (int64_t(lay.rows) * int64_t(kv->live.size()) > INT32_MAX) return fail(UF_ERR_ARG, "shape too large");
+  uf::BwdArgs a{};
+  a.q = f.q;
+  a.o = f.o;
+  a.dout = static_cast<const uint16_t*>(d_do);
+  a.lse = d_lse;
+  a.pool = kv->pool;
+  a.counts = f.counts;
+  a.idx = f.idx;
+  a.mask = reinterpret_cast<const uint32_t*>(static_cast<const uint8_t*>(d_lists) + lay.mask_offset);
+  a.dq = d_dq;
+  a.dk = d_dk;
+  a.dv = d_dv;
+  a.work = static_cast<uint8_t*>(d_work);
+  a.B = f.B;
+  a.H = f.H;
+  a.L = f.L;
+  a.T = f.T;
+  a.NT = f.NT;
+  a.tail = f.tail;
+  a.nk = f.nk;
+  a.nk_cap = f.nk_cap;
+  a.mask_words = int32_t(lay.mask_words);
+  a.n_live = int32_t(kv->live.size());
+  a.scale = f.scale;
+  a.scale_log2 = f.scale_log2;
+  for (int p = 0; p < a.n_live; ++p) a.slot_of[p] = f.slot_of[p];
+  a.tv = f.tv;
+  hipError_t e = uf::launch_attn_bwd(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_bwd launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int uf_block_geom_tokens(const uf_block_geom* g, int32_t* padded_tokens, int32_t* n_blocks) {
   if (int s = check_geom(g, padded_tokens, n_blocks)) return s;
   return ok();

@@ -151,3 +151,24 @@ class KVWindow:
         else:
             L.uf_sparse_causal_attn_fwd(self.handle, q, buf, scale, out, lse_t, stream)
         return (out, lse_t) if lse_t is not None else out
+
+    def attention_bwd(self, q, o, lse, do, scale=None, lists=None, stream=None, work=None):
+        """(dQ [B,L,H,D], dK, dV [n_live,B,L,H,D]) fp32 of the attention of the
+        current chunk, from the forward's O and LSE on the same lists."""
+        for t, name in ((q, "q"), (o, "o"), (do, "do")):
+            _check_chunk(t, name, self.B, self.L, self.H, self.D)
+        if lse.dtype != torch.float32 or tuple(lse.shape) != (self.B, self.H, self.L) or not lse.is_contiguous():
+            raise ValueError("lse must be a contiguous float32 [B, H, L] tensor")
+        if scale is None:
+            scale = 1.0 / math.sqrt(self.D)
+        buf = self.lists if lists is None else lists
+        if buf.numel() < self.layout.total_bytes:
+            raise ValueError("list buffer too small")
+        n_live = self.info().n_live
+        dq = torch.empty((self.B, self.L, self.H, self.D), dtype=torch.float32, device=q.device)
+        dk = torch.empty((n_live, self.B, self.L, self.H, self.D), dtype=torch.float32, device=q.device)
+        dv = torch.empty_like(dk)
+        if work is None:
+            work = torch.empty(L.uf_attn_bwd_work_bytes(self.handle), dtype=torch.uint8, device=q.device)
+        L.uf_sparse_causal_attn_bwd(self.handle, q, o, do, lse, buf, scale, dq, dk, dv, work, None, stream)
+        return dq, dk, dv

@@ -80,7 +80,7 @@ WORKLOADS = {
                           stream_chunks=12),
 }
 
-TENSOR_ID = {"q": 0, "k": 1, "v": 2}
+TENSOR_ID = {"q": 0, "k": 1, "v": 2, "do": 3}
 
 
 def derive_seed(*key: int) -> int:

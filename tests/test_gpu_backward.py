@@ -1,0 +1,169 @@
+"""GPU backward (uf_sparse_causal_attn_bwd through the C ABI) against the CPU
+oracle on the same seeded inputs.
+
+Bar: per (tensor, b, h), ||g_gpu - g_ref||_F / ||g_ref||_F <= 1e-2 for dQ,
+dK and dV.  Derivation: Q, K, V and dO are bf16 inputs, exact on both sides;
+the kernels round P and dS to bf16 (relative 2^-9) before the products that
+give dV, dK and dQ, and take delta from the bf16 forward output, all with fp32
+accumulation.  The rounding errors are independent across terms, so the
+normwise error stays a small multiple of 2^-9 = 2.0e-3; 1e-2 leaves that
+margin and equals the forward's bar.  Keys that no row keeps must get exactly
+zero.  Full comparison at sizes the oracle finishes in seconds (ragged tails,
+batch 2, evictions, a one-token chunk) and on two heads of the 480p window;
+at the 1K window (the launch that bench.py times) sampled dQ rows against the
+oracle and, on every head, identities that the exact gradients satisfy at any
+size.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_common import Case, f64, log, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+GRAD_TOL = 1e-2
+
+
+def _normwise(g, r):
+    den = np.linalg.norm(r)
+    if den == 0:
+        return float(np.linalg.norm(g))
+    return float(np.linalg.norm(g - r) / den)
+
+
+def _run(case, rule, scale=None):
+    scale = 1 / math.sqrt(128) if scale is None else scale
+    case.gpu_lists(rule)
+    q = case.query()
+    o, lse = case.win.attention(q, scale)
+    do = case._draw(case.n_appended - 1, "do")
+    dq, dk, dv = case.win.attention_bwd(q, o, lse, do, scale)
+    torch.cuda.synchronize()
+    return q, o, lse, do, dq, dk, dv
+
+
+def _full_compare(case, rule, heads=None, scale=None):
+    scale = 1 / math.sqrt(128) if scale is None else scale
+    q, o, lse, do, dq, dk, dv = _run(case, rule, scale)
+    bits = case.oracle_bits(rule)
+    hsel = list(range(case.H)) if heads is None else heads
+    bits = bits[:, hsel]
+    rq, rk, rv = oracle.sparse_causal_attention_bwd(case.ring, case._host(q), case._host(do), bits, case.T, scale)
+    gq, gk, gv = dq.cpu().numpy(), dk.cpu().numpy(), dv.cpu().numpy()
+    worst = {"dq": 0.0, "dk": 0.0, "dv": 0.0}
+    for b in range(case.B):
+        for n, h in enumerate(hsel):
+            worst["dq"] = max(worst["dq"], _normwise(gq[b, :, h], rq[b, :, n]))
+            worst["dk"] = max(worst["dk"], _normwise(gk[:, b, :, h], rk[:, b, :, n]))
+            worst["dv"] = max(worst["dv"], _normwise(gv[:, b, :, h], rv[:, b, :, n]))
+            # keys of tiles that no row keeps: exactly zero
+            zero = np.all(rv[:, b, :, n] == 0, axis=-1)
+            assert np.all(gk[:, b, :, h][zero] == 0) and np.all(gv[:, b, :, h][zero] == 0)
+    log("  " + " ".join(f"{k}={v:.3e}" for k, v in worst.items()))
+    assert max(worst.values()) <= GRAD_TOL
+    return dq, dk, dv
+
+
+SMALL = [
+    # B, L, H, max_chunks, pin_sink, n_chunks, p
+    (2, 300, 3, 4, True, 6, 0.5),
+    (1, 1, 1, 3, True, 3, 0.5),
+    (1, 1000, 2, 5, True, 7, 0.25),
+    (1, 256, 1, 1, False, 1, 0.0),
+    (1, 640, 4, 3, False, 4, 0.0),
+    (1, 700, 2, 5, False, 5, 1.0),
+]
+
+
+@pytest.mark.parametrize("B,L,H,mc,pin,n,p", SMALL)
+def test_small_backward_parity(B, L, H, mc, pin, n, p):
+    P = require_gpu()
+    log(f"bwd small B={B} L={L} H={H} max={mc} pin={pin} n={n} p={p}")
+    case = Case(P, B, L, H, 128, mc, pin, seed=2000 + L + H)
+    for _ in range(n):
+        case.append()
+    _full_compare(case, case.rule(p))
+
+
+def test_backward_large_logits():
+    """Peaked rows (q and k scaled by 3): P near one-hot, delta near dP."""
+    P = require_gpu()
+    log("bwd large logits")
+    case = Case(P, 1, 500, 2, 128, 4, True, seed=2101, gain=lambda c, n: 3.0 if n in ("q", "k") else 1.0)
+    for _ in range(4):
+        case.append()
+    _full_compare(case, case.rule(0.5))
+
+
+def test_backward_poisoned_padding_and_determinism():
+    """Padding keys (bf16 9984.0 in the pool) never count, bit for bit, and two
+    runs give identical gradients (no atomics)."""
+    P = require_gpu()
+    log("bwd poison pad + determinism")
+    outs = []
+    for flags in (0, P._lib.UF_F_POISON_PAD):
+        case = Case(P, 1, 300, 2, 128, 3, True, seed=2102, flags=flags)
+        for _ in range(3):
+            case.append()
+        outs.append(_run(case, case.rule(0.5))[4:])
+        outs.append(_run(case, case.rule(0.5))[4:])
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a, b)
+    for a, b in zip(outs[0], outs[2]):
+        assert torch.equal(a, b)
+
+
+def test_backward_480p_full_two_heads():
+    P = require_gpu()
+    wl = synth.WORKLOADS["480p"]
+    log("bwd workload=480p heads 0, 7")
+    case = Case(P, 1, wl.chunk_tokens, wl.heads, wl.tile, wl.max_chunks, wl.pin_sink, wl.seed,
+                gen_device="cuda", oracle_heads=[0, 7])
+    for _ in range(wl.window_chunks):
+        case.append()
+    _full_compare(case, case.rule(wl.p_prior), heads=[0, 7])
+
+
+def test_backward_1k_sampled_rows_and_identities():
+    P = require_gpu()
+    wl = synth.WORKLOADS["1k"]
+    log("bwd workload=1k sampled + identities")
+    case = Case(P, 1, wl.chunk_tokens, wl.heads, wl.tile, wl.max_chunks, wl.pin_sink, wl.seed, gen_device="cuda")
+    for _ in range(wl.window_chunks):
+        case.append()
+    rule = case.rule(wl.p_prior)
+    scale = 1 / math.sqrt(128)
+    q, o, lse, do, dq, dk, dv = _run(case, rule, scale)
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t).all()
+    bits = case.oracle_bits(rule)
+    rng = np.random.default_rng(wl.seed + 7)
+    L, T = wl.chunk_tokens, wl.tile
+    samples = [(0, h, int(r)) for h in range(wl.heads)
+               for r in sorted(set([0, T - 1, T, L - 1, L // 2] + list(rng.integers(0, L, 4))))]
+    hq, hdo = f64(q), f64(do)
+    want = oracle.sparse_causal_attention_bwd_rows(case.ring, hq, hdo, bits, T, scale, samples)
+    gq = dq.cpu().numpy()
+    got = np.stack([gq[b, r, h] for b, h, r in samples])
+    err = max(_normwise(g, w) for g, w in zip(got, want))
+    log(f"  sampled dq rows={len(samples)} worst row normwise={err:.3e}")
+    assert err <= GRAD_TOL
+    # identities of the exact gradients, per head, over the whole window
+    gk, gv, go = dk.cpu().numpy(), dv.cpu().numpy(), f64(o)
+    ks = np.stack([c.k[0] for c in case.ring.logical_chunks()])     # [n_live, L, H, D]
+    vs = np.stack([c.v[0] for c in case.ring.logical_chunks()])
+    for h in range(wl.heads):
+        s_dk = np.linalg.norm(gk[:, 0, :, h].sum(axis=(0, 1)))
+        assert s_dk <= GRAD_TOL * np.linalg.norm(gk[:, 0, :, h])
+        tk = (gk[:, 0, :, h] * ks[:, :, h]).sum(-1)
+        tq = (gq[0, :, h] * hq[0, :, h]).sum(-1)
+        assert abs(tk.sum() - tq.sum()) <= GRAD_TOL * (np.abs(tk).sum() + np.abs(tq).sum())
+        tv = (gv[:, 0, :, h] * vs[:, :, h]).sum(-1)
+        to = (hdo[0, :, h] * go[0, :, h]).sum(-1)
+        assert abs(tv.sum() - to.sum()) <= GRAD_TOL * (np.abs(tv).sum() + np.abs(to).sum())

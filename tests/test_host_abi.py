@@ -34,7 +34,7 @@ def _declared():
 def test_library_exports_every_declared_symbol(P):
     from paper_2606_09150_amd import _lib
     names = _declared()
-    assert len(names) == 21
+    assert len(names) == 23
     lib = ctypes.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -251,3 +251,29 @@ def test_split_kv_host_paths(P):
     assert status(L.uf_attn_split_work_bytes, w64.handle, 2) == L.UF_ERR_UNSUPPORTED
     assert status(L.uf_sparse_causal_attn_fwd_split, w64.handle, None, None, 0.1, None, None, 2, None, 0) == \
         L.UF_ERR_UNSUPPORTED
+
+
+def test_backward_host_paths(P):
+    L = P._lib
+    E = P.UfError
+
+    def status(fn, *a):
+        with pytest.raises(E) as ei:
+            fn(*a)
+        return ei.value.status
+
+    w = _dry(P, max_chunks=4, L=300, T=128, H=2)
+    rows = 2 * 3
+    # per row: Q, Q^T, dO, dO^T (32 KB each) + LSE and delta; per window tile: K^T and V
+    assert L.uf_attn_bwd_work_bytes(w.handle) == rows * (4 * 32768 + 1024) + 4 * rows * 2 * 32768
+    bwd = L.uf_sparse_causal_attn_bwd
+    args = (None, None, None, None, None, 0.1, None, None, None, None, 0)
+    assert status(bwd, w.handle, *args) == L.UF_ERR_EMPTY
+    w.append(None, None)
+    bwd(w.handle, *args)                                                   # dry run: no device work
+    for bad in (0.0, -1.0, float("inf"), float("nan")):
+        assert status(bwd, w.handle, None, None, None, None, None, bad, None, None, None, None, 0) == L.UF_ERR_ARG
+    w64 = _dry(P, max_chunks=2, L=300, T=64)
+    w64.append(None, None)
+    assert status(L.uf_attn_bwd_work_bytes, w64.handle) == L.UF_ERR_UNSUPPORTED
+    assert status(bwd, w64.handle, *args) == L.UF_ERR_UNSUPPORTED

@@ -104,3 +104,39 @@ def test_backward_closed_forms():
     bits3[..., 4] = True
     _, dk3, dv3 = oracle.sparse_causal_attention_bwd(ring2, q2, do2, bits3, T, 0.5)
     assert np.all(dk3[0] == 0) and np.all(dv3[0] == 0) and np.any(dv3[1] != 0)
+
+
+def test_backward_identities():
+    """Properties of the exact gradients at any size: rows of dS sum to zero,
+    so the dK of a head sum to zero over the window's keys; sum_c <dK_c, k_c>
+    = sum_r <dQ_r, q_r> (both equal sum dS * S); sum_c <dV_c, v_c> =
+    sum_r <dO_r, O_r>."""
+    B, L, H, D, T = 2, 9, 2, 6, 4
+    ring, q, do, rng = _ring(B, L, H, D, 3, True, 5)
+    nt = 3
+    bits = _bits(rng, B, H, nt, 3 * nt)
+    scale = 0.4
+    dq, dk, dv = oracle.sparse_causal_attention_bwd(ring, q, do, bits, T, scale)
+    O, _ = oracle.sparse_causal_attention(ring, q, bits, T, scale)
+    ks = np.stack([c.k for c in ring.logical_chunks()])
+    vs = np.stack([c.v for c in ring.logical_chunks()])
+    for b in range(B):
+        for h in range(H):
+            assert np.allclose(dk[:, b, :, h].sum(axis=(0, 1)), 0, atol=1e-12)
+            lhs = (dk[:, b, :, h] * ks[:, b, :, h]).sum()
+            assert np.isclose(lhs, (dq[b, :, h] * q[b, :, h]).sum(), atol=1e-12)
+            assert np.isclose((dv[:, b, :, h] * vs[:, b, :, h]).sum(), (do[b, :, h] * O[b, :, h]).sum(), atol=1e-12)
+
+
+def test_sampled_rows_match_full_backward():
+    B, L, H, D, T = 2, 10, 2, 5, 4
+    ring, q, do, rng = _ring(B, L, H, D, 3, False, 6)
+    nt = 3
+    bits = _bits(rng, B, H, nt, 3 * nt)
+    bits[1, 0, 2] = False                    # a row with no kept tile: zero gradient
+    dq, _, _ = oracle.sparse_causal_attention_bwd(ring, q, do, bits, T, 0.3)
+    samples = [(0, 0, 0), (0, 1, 9), (1, 0, 3), (1, 0, 8), (1, 1, 5)]
+    got = oracle.sparse_causal_attention_bwd_rows(ring, q, do, bits, T, 0.3, samples)
+    want = np.stack([dq[b, r, h] for b, h, r in samples])
+    assert np.allclose(got, want, atol=1e-12)
+    assert np.all(got[3] == 0)
