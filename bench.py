@@ -166,7 +166,7 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     budget = int(wl.p_prior * wl.prior_chunks * nt)
     q_cur = srcs[(wl.window_chunks - 1 + total - 1) % n_src]["q"]
     tk = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    win.lists = lists[0]
+    win.lists = torch.empty_like(lists[0])
     for _ in range(2):
         win.build_topk_lists(q_cur, budget)
     tk[0].record(stream)
@@ -176,8 +176,50 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     torch.cuda.synchronize()
     res["topk_budget"] = budget
     res["topk_lists_us"] = tk[0].elapsed_time(tk[1]) / 10 * 1e3
-    state = {"win": win, "srcs": srcs, "n_src": n_src, "steps_done": total}
+    last = total - 1
+    win.lists = lists[last]
+    state = {"win": win, "srcs": srcs, "n_src": n_src, "steps_done": total, "out": out, "lse": lse,
+             "q": srcs[(wl.window_chunks - 1 + last) % n_src]["q"], "kept_flops": fl[-1][0], "scale": scale}
     return res, state
+
+
+def run_backward(P, wl, state, reps=10, warmup=2):
+    """dQ, dK, dV of the last step's attention (same window, lists, O and LSE).
+
+    FLOPs are counted as the algorithmic backward over the kept (query, key)
+    pairs: five D-long products per pair (S, dP, dV, dK, dQ), i.e. 2.5 times
+    the forward's 4*D; the kernels recompute S and dP once more in the dQ pass
+    (seven products per pair), which the count does not credit."""
+    import torch
+    import synth
+
+    win = state["win"]
+    dev = state["q"].device
+    B, L, H = wl.batch, wl.chunk_tokens, wl.heads
+    n_live = win.info().n_live
+    do = synth.chunk_tensor(wl, 1000, "do", device="cuda")
+    dq = torch.empty((B, L, H, D), dtype=torch.float32, device=dev)
+    dk = torch.empty((n_live, B, L, H, D), dtype=torch.float32, device=dev)
+    dv = torch.empty_like(dk)
+    work = torch.empty(P.uf_attn_bwd_work_bytes(win.handle), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def once():
+        P.uf_sparse_causal_attn_bwd(win.handle, state["q"], state["out"], do, state["lse"], win.lists,
+                                    state["scale"], dq, dk, dv, work, None, stream)
+
+    for _ in range(warmup):
+        once()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record(stream)
+    for _ in range(reps):
+        once()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    flops = state["kept_flops"] * 10 // 4
+    return {"bwd_ms": ms, "bwd_tflop": flops / 1e12, "bwd_tflops": flops / (ms * 1e-3) / 1e12,
+            "bwd_work_bytes": work.numel(), "bwd_reps": reps}
 
 
 def run_blocked(P, wl, steps, warmup, local_r=9, block=(2, 8, 8), n_src=3):
@@ -374,6 +416,7 @@ def main():
                     help="split-KV attention with this many list slices per row (0: whole rows)")
     ap.add_argument("--blocks", action="store_true",
                     help="also run the workload on (2, 8, 8) blocks with the local window r = 9")
+    ap.add_argument("--no-bwd", action="store_true", help="skip timing the backward (dQ, dK, dV)")
     ap.add_argument("--sweep", action="store_true",
                     help="also time the attention against sparsity (top-k lists, no forced chunks)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -433,6 +476,8 @@ def main():
         "frac": res["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS,
         "traffic": measured_traffic(wl.name),
     }
+    if not args.no_bwd:
+        line["backward"] = run_backward(P, wl, state)
     if args.sweep:
         line["sweep"] = sparsity_sweep(wl, state)
     if args.blocks:

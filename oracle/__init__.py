@@ -61,6 +61,7 @@ from .blocks import (
     block_means,
     local_mask,
     attention_in_raster,
+    attention_in_raster_bwd,
 )
 from .backward import sparse_causal_attention_bwd, sparse_causal_attention_bwd_rows
 from .attention import (
@@ -85,6 +86,7 @@ __all__ = [
     "block_means",
     "local_mask",
     "attention_in_raster",
+    "attention_in_raster_bwd",
     "TopkRule",
     "topk_budget",
     "pooled_means",

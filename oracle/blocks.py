@@ -143,3 +143,34 @@ def block_means(x, g: BlockGeom) -> np.ndarray:
         acc = (acc + rows).astype(np.float32)
     n = g.valid_counts().astype(np.float32)[:, None]
     return (acc / n).astype(np.float32)
+
+
+def attention_in_raster_bwd(chunks_k, chunks_v, q, do, g: BlockGeom, bits, scale: float):
+    """Gradients of ``attention_in_raster`` for an upstream gradient do [tokens, D]:
+    per query block, the kept tokens' softmax P, delta = <do, o>, dS = P (do V^T -
+    delta); dq = scale dS K, dK += scale dS^T q, dV += P^T do (float64).
+    Returns (dq [tokens, D], dk list, dv list) with the chunks' shapes."""
+    nb = g.n_blocks
+    blk = block_of_token(g)
+    K = np.concatenate(chunks_k, axis=0)
+    V = np.concatenate(chunks_v, axis=0)
+    key_block = np.concatenate([pos * nb + blk for pos in range(len(chunks_k))])
+    dq = np.zeros_like(q, dtype=np.float64)
+    dK = np.zeros_like(K, dtype=np.float64)
+    dV = np.zeros_like(V, dtype=np.float64)
+    for i in range(nb):
+        rows = np.nonzero(blk == i)[0]
+        cols = np.nonzero(bits[i][key_block])[0]
+        if rows.size == 0 or cols.size == 0:
+            continue
+        S = (q[rows] @ K[cols].T) * scale
+        P = np.exp(S - S.max(axis=1, keepdims=True))
+        P /= P.sum(axis=1, keepdims=True)
+        O = P @ V[cols]
+        dP = do[rows] @ V[cols].T
+        dS = P * (dP - (do[rows] * O).sum(axis=1, keepdims=True))
+        dq[rows] = scale * (dS @ K[cols])
+        dK[cols] += scale * (dS.T @ q[rows])
+        dV[cols] += P.T @ do[rows]
+    n = chunks_k[0].shape[0]
+    return dq, [dK[p * n:(p + 1) * n] for p in range(len(chunks_k))], [dV[p * n:(p + 1) * n] for p in range(len(chunks_k))]

@@ -92,3 +92,37 @@ def test_block_means_float32_rule():
     row = np.float32([1.5, -2.25, 3.0])
     eq = oracle.block_means(np.tile(row, (g.tokens, 1)), g)
     assert np.array_equal(eq, np.tile(row, (g.n_blocks, 1)))
+
+
+def test_attention_in_raster_bwd_central_differences():
+    """Gradients of raster-order block attention against central differences
+    of attention_in_raster, with a partial block set and the local mask."""
+    rng = np.random.default_rng(8)
+    g = oracle.BlockGeom(3, 3, 5, 2, 2, 2)
+    D, nb = 3, g.n_blocks
+    ks = [_rand((g.tokens, D), rng) for _ in range(2)]
+    vs = [_rand((g.tokens, D), rng) for _ in range(2)]
+    q = _rand((g.tokens, D), rng)
+    do = _rand((g.tokens, D), rng)
+    bits = (rng.random((nb, 2 * nb)) < 0.5) & np.tile(oracle.local_mask(g, 3), (1, 2))
+    bits[nb - 1] = False                            # a query block with no kept block
+    scale = 0.6
+    dq, dk, dv = oracle.attention_in_raster_bwd(ks, vs, q, do, g, bits, scale)
+
+    def f():
+        O, _ = oracle.attention_in_raster(ks, vs, q, g, bits, scale)
+        return float((O * do).sum())
+
+    eps = 1e-6
+    for arr, grad in [(q, dq), (ks[0], dk[0]), (ks[1], dk[1]), (vs[0], dv[0]), (vs[1], dv[1])]:
+        num = np.zeros_like(arr)
+        for idx in np.ndindex(arr.shape):
+            keep = arr[idx]
+            arr[idx] = keep + eps
+            fp = f()
+            arr[idx] = keep - eps
+            fm = f()
+            arr[idx] = keep
+            num[idx] = (fp - fm) / (2 * eps)
+        assert np.allclose(grad, num, atol=1e-7, rtol=1e-6)
+    assert np.all(dq[oracle.block_of_token(g) == nb - 1] == 0)
