@@ -7,24 +7,26 @@
 // delta = <dO, O>, dS = P (dO V^T - delta):
 //   dV = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K.
 //
-// Four kernels, all with 32x32x16 bf16 MFMA and fp32 accumulation:
-//  * prep_queries: per query tile, Q and dO row-major and transposed (query
-//    index in swap23 order within groups of 16, the k-slot order of the MFMA
-//    result lanes), LSE*log2(e) (+inf for rows past the chunk end, so that their
-//    weights vanish) and delta;
-//  * prep_keys: per window key tile, K^T (keys in swap23 order) and V
-//    row-major, from the pool's K rows and V^T columns;
-//  * dkdv: one workgroup per window key tile, four waves of 32 keys; it walks
-//    the query tiles whose lists keep the tile (mask bits), and per 32-query
-//    block computes S = Q K^T (keys on the result lanes), P, dP = dO V^T,
-//    dS, then dV^T += dO^T P and dK^T += Q^T dS with P and dS used in place as
-//    B operands;
+// Three kernels, all with 32x32x16 bf16 MFMA and fp32 accumulation:
+//  * prep: per query tile, Q and dO rows (rows past the chunk end zero),
+//    LSE*log2(e) (+inf on those rows, so that their weights vanish) and delta;
+//  * dkdv: per window key tile, one workgroup accumulating dK and (a second
+//    launch) one accumulating dV, four waves of 32 keys each; they walk the query tiles whose lists keep
+//    the tile (mask bits) and per 32-query block compute S = Q K^T (keys on the
+//    result lanes), P (and dP = dO V^T, dS), then dV^T += dO^T P or
+//    dK^T += Q^T dS with P or dS used in place as the B operand;
 //  * dq: one workgroup per query tile, four waves of 32 queries; it walks the
-//    row's list and per 32-key block computes S^T = K Q^T (queries on the
-//    lanes), P^T, dP^T = V dO^T, dS^T, then dQ^T += K^T dS^T.
-// No atomics: every output row is owned by one workgroup, so results are
-// reproducible.  Tiles stream into LDS by direct global->LDS copies with the
-// same XOR swizzle as the forward; the loops are single-buffered.
+//    row's list and per 32-key block computes S^T = K Q^T, dP^T = V dO^T, dS^T,
+//    then dQ^T += K^T dS^T.
+// The transposed operands (dO^T, Q^T, K^T, and V rows from the pool's V^T)
+// come from row-major LDS tiles through the transposing LDS read
+// (ds_read_b64_tr_b16), so each tile is copied into LDS once, in the layout the
+// pool or the workspace already holds.  Each workgroup needs at most 73 KB of
+// LDS and 256 registers per lane, so two run on every CU and one's copies
+// overlap the other's products.  No atomics: every output row is owned by one
+// workgroup, so results are reproducible.
+#include <type_traits>
+
 #include "attn_common.h"
 
 namespace uf {
@@ -35,52 +37,36 @@ using namespace attn;
 constexpr int kT = 128;
 constexpr int kThreads = 256;                  // four waves
 constexpr uint32_t kTile = 32768;              // one [128][128] bf16 tile
-constexpr int kStage = 17;                     // padded LDS row stride in 16-byte chunks
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 __device__ inline float bf16f(uint16_t x) { return __uint_as_float(uint32_t(x) << 16); }
-__device__ inline uint16_t f2bf(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
 // ---------------------------------------------------------------- prep ----
 
-// Row-major copy of one query tile of x [B, L, H, D] into dst (rows past the
-// chunk end zero) and into an LDS stage; then the transposed tile.
-__device__ void tile_both_ways(const uint16_t* x, int b, int h, int i, int nv, const BwdArgs& a, uint4* stage,
-                               uint4* dst_rows, uint4* dst_t) {
-  for (int c = threadIdx.x; c < kT * 16; c += kThreads) {
-    const int r = c >> 4, cc = c & 15;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < nv) v = *reinterpret_cast<const uint4*>(x + ((size_t(b) * a.L + size_t(i) * kT + r) * a.H + h) * kD + cc * 8);
-    dst_rows[c] = v;
-    stage[r * kStage + cc] = v;
-  }
-  __syncthreads();
-  const uint16_t* st = reinterpret_cast<const uint16_t*>(stage);
-  for (int c = threadIdx.x; c < kD * 16; c += kThreads) {
-    const int d = c >> 4, p0 = (c & 15) * 8;
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t lo = st[swap23(p0 + 2 * e) * (kStage * 8) + d];
-      const uint32_t hi = st[swap23(p0 + 2 * e + 1) * (kStage * 8) + d];
-      w[e] = lo | (hi << 16);
-    }
-    dst_t[c] = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-  __syncthreads();
-}
-
-__global__ __launch_bounds__(kThreads) void bwd_prep_queries_kernel(BwdArgs a) {
-  __shared__ uint4 stage[kT * kStage];
+__global__ __launch_bounds__(kThreads) void bwd_prep_kernel(BwdArgs a) {
   const int row = blockIdx.x;                  // (b*H + h)*NT + i
   const int i = row % a.NT;
   const int bh = row / a.NT;
   const int h = bh % a.H, b = bh / a.H;
   const int nv = tile_valid(a.tv, i, a.NT, a.tail, kT);
-  uint8_t* qt = a.work + size_t(row) * kBwdQTile;
-  tile_both_ways(a.q, b, h, i, nv, a, stage, reinterpret_cast<uint4*>(qt), reinterpret_cast<uint4*>(qt + kTile));
-  tile_both_ways(a.dout, b, h, i, nv, a, stage, reinterpret_cast<uint4*>(qt + 2 * kTile),
-                 reinterpret_cast<uint4*>(qt + 3 * kTile));
-  float* lse2 = reinterpret_cast<float*>(qt + 4 * kTile);
+  uint8_t* rec = a.work + size_t(row) * kBwdQTile;
+  uint4* qr = reinterpret_cast<uint4*>(rec);
+  uint4* orow = reinterpret_cast<uint4*>(rec + kTile);
+  for (int c = threadIdx.x; c < kT * 16; c += kThreads) {
+    const int r = c >> 4, cc = c & 15;
+    uint4 vq = make_uint4(0, 0, 0, 0), vo = vq;
+    if (r < nv) {
+      const size_t off = ((size_t(b) * a.L + size_t(i) * kT + r) * a.H + h) * kD + cc * 8;
+      vq = *reinterpret_cast<const uint4*>(a.q + off);
+      vo = *reinterpret_cast<const uint4*>(a.dout + off);
+    }
+    qr[c] = vq;
+    orow[c] = vo;
+  }
+  float* lse2 = reinterpret_cast<float*>(rec + 2 * kTile);
   float* delta = lse2 + kT;
   if (threadIdx.x < kT) {
     const int q = threadIdx.x;
@@ -97,74 +83,60 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_queries_kernel(BwdArgs a) {
   }
 }
 
-__global__ __launch_bounds__(kThreads) void bwd_prep_keys_kernel(BwdArgs a) {
-  __shared__ uint4 stage[kT * kStage];
-  const int kj = blockIdx.x;                   // ((pos*B + b)*H + h)*NT + t
-  const int t = kj % a.NT;
-  const int posbh = kj / a.NT;
-  const int bh = posbh % (a.B * a.H);
-  const int pos = posbh / (a.B * a.H);
-  const uint8_t* page = a.pool + ((size_t(a.slot_of[pos]) * a.B * a.H + bh) * a.NT + t) * page_bytes(kT, kD);
-  uint8_t* kt = a.work + size_t(a.B) * a.H * a.NT * kBwdQTile + size_t(kj) * kBwdKTile;
-  const uint4* krows = reinterpret_cast<const uint4*>(page);
-  const uint4* vt = reinterpret_cast<const uint4*>(page + kTile);
-  // K^T: stage the K rows, write columns with keys in swap23 order
-  for (int c = threadIdx.x; c < kT * 16; c += kThreads) stage[(c >> 4) * kStage + (c & 15)] = krows[c];
-  __syncthreads();
-  const uint16_t* st = reinterpret_cast<const uint16_t*>(stage);
-  uint4* dst = reinterpret_cast<uint4*>(kt);
-  for (int c = threadIdx.x; c < kD * 16; c += kThreads) {
-    const int d = c >> 4, p0 = (c & 15) * 8;
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t lo = st[swap23(p0 + 2 * e) * (kStage * 8) + d];
-      const uint32_t hi = st[swap23(p0 + 2 * e + 1) * (kStage * 8) + d];
-      w[e] = lo | (hi << 16);
-    }
-    dst[c] = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-  __syncthreads();
-  // V rows: V^T row d holds key swap23(p) at column p
-  for (int c = threadIdx.x; c < kD * 16; c += kThreads) stage[(c >> 4) * kStage + (c & 15)] = vt[c];
-  __syncthreads();
-  dst = reinterpret_cast<uint4*>(kt + kTile);
-  for (int c = threadIdx.x; c < kT * 16; c += kThreads) {
-    const int key = c >> 4, d0 = (c & 15) * 8;
-    const int p = swap23(key);
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t lo = st[(d0 + 2 * e) * (kStage * 8) + p];
-      const uint32_t hi = st[(d0 + 2 * e + 1) * (kStage * 8) + p];
-      w[e] = lo | (hi << 16);
-    }
-    dst[c] = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-}
-
 // ------------------------------------------------------------- shared ----
 
-// Copy one 32 KB tile global -> LDS with the forward's XOR swizzle (chunk c of
-// row r lands at r*16 + (c ^ (r & 15))): eight 16-byte copies per wave.
-__device__ inline void copy_tile(const uint8_t* src, uint32_t lds_tile, int wave, int lane) {
+// LDS layout of a [128][128] bf16 tile: 16-byte chunk c of row r sits at
+// position perm(c) ^ f(r) of the row, perm swapping bits 1 and 3 of c and
+// f(r) = (r3, r1, r0, r2 ^ r3) (bits 3..0).  Both 16-byte row reads (eight or
+// sixteen consecutive rows, or rows in swap23 order, one chunk) and the
+// transposing 8-byte reads (four consecutive rows, four consecutive chunks
+// per 32 lanes) then touch every bank once per cycle, with 32 or 64 banks.
+__device__ inline int swz_perm(int c) { return (c & ~10) | ((c & 2) << 2) | ((c & 8) >> 2); }
+__device__ inline int swz_f(int r) { return (r & 8) | ((r & 3) << 1) | (((r >> 2) ^ (r >> 3)) & 1); }
+
+// Copy one 32 KB tile global -> LDS in that layout: copy i of wave w fills
+// LDS chunks [64*(4i + w), +64), i.e. row 16i + 4w + lane/16, position
+// lane%16.  The row's low four bits do not depend on i, so one per-lane
+// source offset serves all eight copies, with 4 KB steps on the scalar base.
+__device__ inline uint32_t copy_offset(int wave, int lane) {
+  const int r = 4 * wave + (lane >> 4);
+  return uint32_t(r * 256 + swz_perm((lane & 15) ^ swz_f(r)) * 16);
+}
+__device__ inline void copy_tile(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int p = (4 * i + wave) * 64 + lane;
-    const int r = p >> 4, cs = p & 15;
-    dma16(src, uint32_t(r * 256 + ((cs ^ (r & 15)) * 16)), lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 4096u);
-  }
+  for (int i = 0; i < 8; ++i) dma16(src + i * 4096, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 4096u);
 }
 
-// LDS byte offset of logical 16-byte chunk c of row r of a swizzled tile.
-__device__ inline uint32_t swz(int r, int c) { return uint32_t(r * 256 + ((c ^ (r & 15)) * 16)); }
+// LDS byte offset of bf16 element (r, c) of a tile.
+__device__ inline uint32_t swz_elem(int r, int c) {
+  return uint32_t(r * 256 + ((swz_perm(c >> 3) ^ swz_f(r & 15)) << 4) + (c & 7) * 2);
+}
 
 __device__ inline bf16x8 lds8(const uint8_t* base, uint32_t off) {
   return as_bf16x8(*reinterpret_cast<const uint4*>(base + off));
 }
 
+// MFMA operand (A or B: lane l holds row/column l%32 and k-slots 8*(l/32)+e)
+// from a swizzled tile stored k-major: tile row krow(kappa) holds k-slot kappa,
+// and the operand's rows/columns are tile columns col0 .. col0+31.  Two
+// transposing reads: in every group of 16 lanes, lane i receives element i%4
+// of the 8-byte pieces read by lanes i/4 + 4k (k = 0..3), so lane r' of group g
+// reads tile row krow(8*hl + 4*h + r'/4), columns col0 + 16g + 4*(r'%4) .. +3.
+template <class KRow>
+__device__ inline bf16x8 tr_operand(const lds_u8* tile, int col0, int lane, KRow krow) {
+  const int rp = lane & 15, g = (lane >> 4) & 1, hl = lane >> 5;
+  const int c = col0 + 16 * g + 4 * (rp & 3);
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4i16*)(tile + swz_elem(krow(8 * hl + (rp >> 2)), c)));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4i16*)(tile + swz_elem(krow(8 * hl + 4 + (rp >> 2)), c)));
+  const v4i16 v[2] = {lo, hi};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
 // bf16 B operand for k-step kk (16 rows of a 32-row MFMA result block) from
-// the fp32 result registers: rows 16kk + 8j + 4hl + i, j in {0, 1}, i in 0..3.
+// the fp32 result registers: rows 16kk + 8j + 4hl + i, j in {0, 1}, i in 0..3,
+// i.e. k-slot kappa holds result row 16kk + swap23(kappa).
 __device__ inline bf16x8 rows_to_operand(const f32x16& x, int kk) {
   bf16x8 r;
 #pragma unroll
@@ -174,11 +146,21 @@ __device__ inline bf16x8 rows_to_operand(const f32x16& x, int kk) {
 
 // ---------------------------------------------------------------- dkdv ----
 
-__global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
-  __shared__ uint4 sQ[kT * 16], sQT[kT * 16], sO[kT * 16], sOT[kT * 16];
-  __shared__ float sL[kT], sDl[kT];
+// Workgroup kj for window key tile kj = ((pos*B + b)*H + h)*NT + t; ROLE 0
+// accumulates dV, ROLE 1 dK (two launches, so that each is compiled for its
+// own register budget).  Lane ln of wave w holds key
+// 32w + swap23(ln): then the V operand read transposed from the pool's V^T
+// tile (whose columns hold the keys in swap23 order) lands in natural lane
+// order.
+template <int ROLE>
+__global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdArgs a) {
+  __shared__ uint4 sQ[kT * 16], sO[kT * 16];    // Q and dO rows of one query tile (64 KB)
+  __shared__ float sLD[2 * kT];                  // LSE*log2(e), then delta
+  __shared__ uint16_t sList[kBwdMaxQTiles];
+  __shared__ int sN;
 
-  const int kj = blockIdx.x;                   // ((pos*B + b)*H + h)*NT + t
+  constexpr int role = ROLE;
+  const int kj = blockIdx.x;
   const int t = kj % a.NT;
   const int posbh = kj / a.NT;
   const int bh = posbh % (a.B * a.H);
@@ -187,80 +169,136 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
+  const uint32_t voff = copy_offset(wave, lane);
   const int kvalid = tile_valid(a.tv, t, a.NT, a.tail, kT);
-  const int key = wave * 32 + ln;               // this lane's key (result column)
+  const int key = wave * 32 + swap23(ln);       // this lane's key (result column)
   const bool key_ok = key < kvalid;
   const int j = pos * a.NT + t;                 // logical key tile
+  const lds_u8* lq = (const lds_u8*)sQ;
+  const lds_u8* lo = (const lds_u8*)sO;
 
-  // the wave's 32 keys as B operands: K rows from the page, V rows from the workspace
+  // the wave's 32 keys as B operands: K rows straight from the page; V rows
+  // (dK only) through LDS, read transposed from the page's V^T
   const uint8_t* page = a.pool + ((size_t(a.slot_of[pos]) * a.B * a.H + bh) * a.NT + t) * page_bytes(kT, kD);
-  const uint8_t* kw = a.work + size_t(a.B) * a.H * a.NT * kBwdQTile + size_t(kj) * kBwdKTile;
   bf16x8 kf[8], vf[8];
 #pragma unroll
-  for (int ks = 0; ks < 8; ++ks) {
+  for (int ks = 0; ks < 8; ++ks)
     kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + size_t(key) * 256 + (2 * ks + hl) * 16));
-    vf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(kw + kTile + size_t(key) * 256 + (2 * ks + hl) * 16));
+  if constexpr (role == 1) copy_tile(page + kTile, lds_addr(sO), voff, wave);
+
+  // kept query tiles, ascending
+  if (wave == 0) {
+    int cnt = 0;
+    for (int base = 0; base < a.NT; base += 512) {
+      uint32_t w[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int i = base + 64 * k + lane;
+        w[k] = i < a.NT ? a.mask[size_t(bh * a.NT + i) * a.mask_words + (j >> 5)] : 0u;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const bool keep = (w[k] >> (j & 31)) & 1u;
+        const uint64_t bal = __ballot(keep);
+        if (keep) sList[cnt + __popcll(bal & ((uint64_t(1) << lane) - 1))] = uint16_t(base + 64 * k + lane);
+        cnt += __popcll(bal);
+      }
+    }
+    if (lane == 0) sN = cnt;
   }
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
-
-  f32x16 dvt[4], dkt[4];                        // [4 dim blocks][32 dims x 32 keys]
+  __syncthreads();
+  if constexpr (role == 1) {
+    // V^T tile row = dim (k-slot 16ks + kappa), columns = key columns 32w ..
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
-    dvt[mb] = f32x16{};
-    dkt[mb] = f32x16{};
+    for (int ks = 0; ks < 8; ++ks) vf[ks] = tr_operand(lo, wave * 32, lane, [&](int kap) { return 16 * ks + kap; });
   }
-  const uint8_t* lq = reinterpret_cast<const uint8_t*>(sQ);
-  const uint8_t* lqt = reinterpret_cast<const uint8_t*>(sQT);
-  const uint8_t* lo = reinterpret_cast<const uint8_t*>(sO);
-  const uint8_t* lot = reinterpret_cast<const uint8_t*>(sOT);
-  const float c2 = a.scale_log2;
+  const int N = __builtin_amdgcn_readfirstlane(sN);
 
-  for (int i = 0; i < a.NT; ++i) {
-    const int row = bh * a.NT + i;
-    const uint32_t word = __builtin_amdgcn_readfirstlane(a.mask[size_t(row) * a.mask_words + (j >> 5)]);
-    if (((word >> (j & 31)) & 1u) == 0) continue;
-    const uint8_t* qt = a.work + size_t(row) * kBwdQTile;
-    __syncthreads();                            // previous tiles consumed
-    copy_tile(qt, lds_addr(sQ), wave, lane);
-    copy_tile(qt + kTile, lds_addr(sQT), wave, lane);
-    copy_tile(qt + 2 * kTile, lds_addr(sO), wave, lane);
-    copy_tile(qt + 3 * kTile, lds_addr(sOT), wave, lane);
-    if (tid < kT) {
-      sL[tid] = reinterpret_cast<const float*>(qt + 4 * kTile)[tid];
-      sDl[tid] = reinterpret_cast<const float*>(qt + 4 * kTile)[kT + tid];
-    }
+  f32x16 acc[4];                                // dV^T or dK^T: [4 dim blocks][32 dims x 32 keys]
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x16{};
+  const float c2 = a.scale_log2;
+  const uint8_t* qbase = a.work + size_t(bh) * a.NT * kBwdQTile;
+
+  // S = Q K^T for 32 queries x the wave's 32 keys
+  auto scores = [&](int qb) {
+    f32x16 sv = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8((const uint8_t*)sQ, swz_elem(qb * 32 + ln, 16 * ks + 8 * hl)),
+                                                   kf[ks], sv, 0, 0, 0);
+    return sv;
+  };
+  // acc^T += X^T op over the block's 32 queries: X (Q or dO rows) read transposed,
+  // k-slot kappa of step kk = query qb*32 + 16kk + swap23(kappa)
+  auto accumulate = [&](const lds_u8* x, int qb, const bf16x8 (&op)[2]) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            tr_operand(x, mb * 32, lane, [&](int kap) { return qb * 32 + 16 * kk + swap23(kap); }), op[kk], acc[mb],
+            0, 0, 0);
+  };
+
+  for (int n = 0; n < N; ++n) {
+    const uint8_t* rec = qbase + size_t(__builtin_amdgcn_readfirstlane(int(sList[n]))) * kBwdQTile;
+    __syncthreads();                            // previous tile consumed
+    copy_tile(rec, lds_addr(sQ), voff, wave);
+    copy_tile(rec + kTile, lds_addr(sO), voff, wave);
+    if (wave == 0) dma16(rec + 2 * kTile, uint32_t(lane) * 16u, lds_addr(sLD));
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
+    if constexpr (role == 0) {
 #pragma unroll 1
-    for (int qb = 0; qb < 4; ++qb) {
-      // S = Q K^T and dP = dO V^T for 32 queries x the wave's 32 keys
-      f32x16 s = f32x16{}, dp = f32x16{};
+      for (int qb = 0; qb < 4; ++qb) {
+        const f32x16 sv = scores(qb);
+        // P; result row r holds query qb*32 + 8*(r/4) + 4*hl + r%4
+        f32x16 p;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const uint32_t off = swz(qb * 32 + ln, 2 * ks + hl);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lq, off), kf[ks], s, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lo, off), vf[ks], dp, 0, 0, 0);
-      }
-      // P and dS; result row r holds query qb*32 + 8*(r/4) + 4*hl + r%4
-      f32x16 p, ds;
+        for (int g = 0; g < 4; ++g) {
+          const float4 l4 = *reinterpret_cast<const float4*>(&sLD[qb * 32 + 8 * g + 4 * hl]);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int q = qb * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-        const float e = __builtin_amdgcn_exp2f(s[r] * c2 - sL[q]);
-        p[r] = key_ok ? e : 0.f;
-        ds[r] = p[r] * (dp[r] - sDl[q]);
-      }
-      // dV^T += dO^T P, dK^T += Q^T dS (k = the block's queries)
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const bf16x8 pb = rows_to_operand(p, kk);
-        const bf16x8 db = rows_to_operand(ds, kk);
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-          const uint32_t off = swz(mb * 32 + ln, 4 * qb + 2 * kk + hl);
-          dvt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lot, off), pb, dvt[mb], 0, 0, 0);
-          dkt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lqt, off), db, dkt[mb], 0, 0, 0);
+          for (int e = 0; e < 4; ++e) {
+            const float w = __builtin_amdgcn_exp2f(sv[4 * g + e] * c2 - lv[e]);
+            p[4 * g + e] = key_ok ? w : 0.f;
+          }
         }
+        const bf16x8 op[2] = {rows_to_operand(p, 0), rows_to_operand(p, 1)};
+        __builtin_amdgcn_sched_barrier(0);       // bound the operand reads in flight
+        accumulate(lo, qb, op);                  // dV^T += dO^T P
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll 1
+      for (int qb = 0; qb < 4; ++qb) {
+        const f32x16 sv = scores(qb);
+        __builtin_amdgcn_sched_barrier(0);       // bound the operand reads in flight
+        f32x16 dpv = f32x16{};
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks)
+          dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              lds8((const uint8_t*)sO, swz_elem(qb * 32 + ln, 16 * ks + 8 * hl)), vf[ks], dpv, 0, 0, 0);
+        f32x16 ds;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int q0 = qb * 32 + 8 * g + 4 * hl;
+          const float4 l4 = *reinterpret_cast<const float4*>(&sLD[q0]);
+          const float4 d4 = *reinterpret_cast<const float4*>(&sLD[kT + q0]);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * g + e;
+            const float w = __builtin_amdgcn_exp2f(sv[r] * c2 - lv[e]);
+            ds[r] = (key_ok ? w : 0.f) * (dpv[r] - dv[e]);
+          }
+        }
+        const bf16x8 op[2] = {rows_to_operand(ds, 0), rows_to_operand(ds, 1)};
+        __builtin_amdgcn_sched_barrier(0);
+        accumulate(lq, qb, op);                  // dK^T += Q^T dS
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
@@ -269,25 +307,26 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   // rows inside the chunk (block order) get the zeros they accumulated
   const size_t tok = size_t(t) * kT + key;
   if (tok < size_t(a.L)) {
-    const size_t base = (((size_t(pos) * a.B + b) * a.L + tok) * a.H + h) * kD;
+    float* dst = (role ? a.dk : a.dv) + (((size_t(pos) * a.B + b) * a.L + tok) * a.H + h) * kD;
+    const float f = role ? a.scale : 1.0f;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int d0 = mb * 32 + 8 * g + 4 * hl;
-        *reinterpret_cast<float4*>(a.dv + base + d0) =
-            make_float4(dvt[mb][4 * g], dvt[mb][4 * g + 1], dvt[mb][4 * g + 2], dvt[mb][4 * g + 3]);
-        *reinterpret_cast<float4*>(a.dk + base + d0) =
-            make_float4(dkt[mb][4 * g] * a.scale, dkt[mb][4 * g + 1] * a.scale, dkt[mb][4 * g + 2] * a.scale,
-                        dkt[mb][4 * g + 3] * a.scale);
-      }
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<float4*>(dst + mb * 32 + 8 * g + 4 * hl) =
+            make_float4(acc[mb][4 * g] * f, acc[mb][4 * g + 1] * f, acc[mb][4 * g + 2] * f, acc[mb][4 * g + 3] * f);
   }
 }
 
 // ------------------------------------------------------------------ dq ----
 
-__global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
-  __shared__ uint4 sK[kT * 16], sV[kT * 16], sKT[kT * 16];
+// One workgroup per query tile.  The S^T and dP^T result rows of key block kb
+// hold keys kb*32 + swap23(m) (m = result row), the order in which the V
+// operand arrives when read transposed from the page's V^T; K rows are read
+// in the same order.  dS^T as a B operand then holds natural key order.
+// Entries naming a tile outside the window count no key.
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
+  __shared__ uint4 sK[kT * 16], sV[kD * 16];    // K rows and V^T of one page (64 KB)
 
   const int row = blockIdx.x;                  // (b*H + h)*NT + i
   const int i = row % a.NT;
@@ -296,71 +335,74 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
+  const uint32_t voff = copy_offset(wave, lane);
   const int q = wave * 32 + ln;                 // this lane's query (result column)
+  const lds_u8* lk = (const lds_u8*)sK;
+  const lds_u8* lv = (const lds_u8*)sV;
 
-  const uint8_t* qt = a.work + size_t(row) * kBwdQTile;
+  const uint8_t* rec = a.work + size_t(row) * kBwdQTile;
   bf16x8 qf[8], of[8];
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks) {
-    qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qt + size_t(q) * 256 + (2 * ks + hl) * 16));
-    of[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qt + 2 * kTile + size_t(q) * 256 + (2 * ks + hl) * 16));
+    qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(rec + size_t(q) * 256 + (2 * ks + hl) * 16));
+    of[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(rec + kTile + size_t(q) * 256 + (2 * ks + hl) * 16));
   }
-  const float l2 = reinterpret_cast<const float*>(qt + 4 * kTile)[q];
-  const float dl = reinterpret_cast<const float*>(qt + 4 * kTile)[kT + q];
+  const float l2 = reinterpret_cast<const float*>(rec + 2 * kTile)[q];
+  const float dl = reinterpret_cast<const float*>(rec + 2 * kTile)[kT + q];
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
   f32x16 dqt[4];                                // [4 dim blocks][32 dims x 32 queries]
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) dqt[mb] = f32x16{};
-  const uint8_t* lk = reinterpret_cast<const uint8_t*>(sK);
-  const uint8_t* lv = reinterpret_cast<const uint8_t*>(sV);
-  const uint8_t* lkt = reinterpret_cast<const uint8_t*>(sKT);
   const float c2 = a.scale_log2;
-  const int count = ((const const_i32*)a.counts)[row];
+  const int N = ((const const_i32*)a.counts)[row];
   const const_i32* list = ((const const_i32*)a.idx) + size_t(row) * a.nk_cap;
-  const uint8_t* kbase = a.work + size_t(a.B) * a.H * a.NT * kBwdQTile;
+  const size_t pbytes = page_bytes(kT, kD);
+  const uint8_t* head_pages = a.pool + size_t(bh) * a.NT * pbytes;
+  const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
 
-  for (int n = 0; n < count; ++n) {
+  for (int n = 0; n < N; ++n) {
     const int j = list[n];
-    if (unsigned(j) >= unsigned(a.nk)) continue;   // outside the window: no key
-    const int pos = j / a.NT;
-    const int t = j - pos * a.NT;
-    const int kvalid = tile_valid(a.tv, t, a.NT, a.tail, kT);
-    const uint8_t* page = a.pool + ((size_t(a.slot_of[pos]) * a.B * a.H + bh) * a.NT + t) * page_bytes(kT, kD);
-    const uint8_t* kw = kbase + ((size_t(pos) * a.B * a.H + bh) * a.NT + t) * kBwdKTile;
-    __syncthreads();                            // previous tiles consumed
-    copy_tile(page, lds_addr(sK), wave, lane);
-    copy_tile(kw + kTile, lds_addr(sV), wave, lane);
-    copy_tile(kw, lds_addr(sKT), wave, lane);
+    int kvalid = 0;
+    const uint8_t* page = head_pages + size_t(a.slot_of[0]) * slot_stride;
+    if (unsigned(j) < unsigned(a.nk)) {
+      const int pos = j / a.NT, t = j - pos * a.NT;
+      kvalid = tile_valid(a.tv, t, a.NT, a.tail, kT);
+      page = head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
+    }
+    __syncthreads();                            // previous tile consumed
+    copy_tile(page, lds_addr(sK), voff, wave);
+    copy_tile(page + kTile, lds_addr(sV), voff, wave);
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
 #pragma unroll 1
     for (int kb = 0; kb < 4; ++kb) {
-      // S^T = K Q^T and dP^T = V dO^T for the block's 32 keys x the wave's 32 queries
-      f32x16 s = f32x16{}, dp = f32x16{};
+      // S^T = K Q^T and dP^T = V dO^T: A operands are K rows kb*32 + swap23(ln)
+      // and V read transposed from V^T (tile row = dim, columns kb*32 ..)
+      f32x16 sv = f32x16{}, dpv = f32x16{};
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const uint32_t off = swz(kb * 32 + ln, 2 * ks + hl);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lk, off), qf[ks], s, 0, 0, 0);
-        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lv, off), of[ks], dp, 0, 0, 0);
+        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds8((const uint8_t*)sK, swz_elem(kb * 32 + swap23(ln), 16 * ks + 8 * hl)), qf[ks], sv, 0, 0, 0);
+        dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            tr_operand(lv, kb * 32, lane, [&](int kap) { return 16 * ks + kap; }), of[ks], dpv, 0, 0, 0);
       }
-      // result row r holds key kb*32 + 8*(r/4) + 4*hl + r%4
+      // result row m = 8*(r/4) + 4*hl + r%4 holds key kb*32 + swap23(m)
       f32x16 ds;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = kb * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-        const float e = __builtin_amdgcn_exp2f(s[r] * c2 - l2);
-        const float pr = key < kvalid ? e : 0.f;
-        ds[r] = pr * (dp[r] - dl);
+        const int key = kb * 32 + swap23(8 * (r >> 2) + 4 * hl + (r & 3));
+        const float e = __builtin_amdgcn_exp2f(sv[r] * c2 - l2);
+        ds[r] = (key < kvalid ? e : 0.f) * (dpv[r] - dl);
       }
-      // dQ^T += K^T dS^T (k = the block's keys)
+      // dQ^T += K^T dS^T: k-slot kappa of step kk = key kb*32 + 16kk + kappa
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         const bf16x8 db = rows_to_operand(ds, kk);
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
-          dqt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(lkt, swz(mb * 32 + ln, 4 * kb + 2 * kk + hl)), db,
-                                                            dqt[mb], 0, 0, 0);
+          dqt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              tr_operand(lk, mb * 32, lane, [&](int kap) { return kb * 32 + 16 * kk + kap; }), db, dqt[mb], 0, 0, 0);
       }
     }
   }
@@ -385,12 +427,12 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(BwdArgs a) {
 hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream) {
   const unsigned qrows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
   const unsigned ktiles = unsigned(a.n_live) * qrows;
-  bwd_prep_queries_kernel<<<qrows, kThreads, 0, stream>>>(a);
+  bwd_prep_kernel<<<qrows, kThreads, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  bwd_prep_keys_kernel<<<ktiles, kThreads, 0, stream>>>(a);
+  bwd_dkdv_kernel<1><<<ktiles, kThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  bwd_dkdv_kernel<<<ktiles, kThreads, 0, stream>>>(a);
+  bwd_dkdv_kernel<0><<<ktiles, kThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   bwd_dq_kernel<<<qrows, kThreads, 0, stream>>>(a);
   return hipGetLastError();

@@ -98,12 +98,10 @@ struct AttnArgs {
 };
 
 // Backward of the attention.  The workspace holds, per query tile (b, h, i),
-// Q and dO row-major and transposed (the query index of the transposed tiles
-// in swap23 order within groups of 16), then LSE*log2(e) and delta = <dO, O>
-// per query; and, per window key tile (logical position, b, h, t), K^T (keys
-// in swap23 order) and V row-major.
-constexpr size_t kBwdQTile = 4 * 32768 + 1024;
-constexpr size_t kBwdKTile = 2 * 32768;
+// the Q and dO rows (zero past the chunk end), then LSE*log2(e) and
+// delta = <dO, O> per query.
+constexpr size_t kBwdQTile = 2 * 32768 + 1024;
+constexpr int kBwdMaxQTiles = 4096;   // query tiles per chunk the backward handles
 struct BwdArgs {
   const uint16_t* q;      // [B, L, H, D]
   const uint16_t* o;      // [B, L, H, D]

@@ -470,13 +470,8 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
 
 namespace {
 
-// Query-tile records for every row, then key-tile records for every window
-// position the handle can hold, so the size does not change as chunks come
-// and go.
-size_t bwd_work_bytes(const uf_kv* kv) {
-  const size_t rows = size_t(kv->layout().rows);
-  return rows * uf::kBwdQTile + size_t(kv->d.max_chunks) * rows * uf::kBwdKTile;
-}
+// One query-tile record per list row.
+size_t bwd_work_bytes(const uf_kv* kv) { return size_t(kv->layout().rows) * uf::kBwdQTile; }
 
 }  // namespace
 
@@ -492,6 +487,7 @@ int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o,
                               float* d_dv, void* d_work, size_t work_bytes, void* stream) {
   if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
   if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "the backward needs 128-token tiles");
+  if (kv->nt > uf::kBwdMaxQTiles) return fail(UF_ERR_UNSUPPORTED, "the backward handles at most %d query tiles", uf::kBwdMaxQTiles);
   uf::AttnArgs f{};
   if (int s = attn_args(kv, d_q, d_lists, scale, const_cast<void*>(d_o), const_cast<float*>(d_lse), &f)) return s;
   if (kv->dry()) return ok();
