@@ -146,20 +146,38 @@ __device__ inline bf16x8 rows_to_operand(const f32x16& x, int kk) {
 
 // ---------------------------------------------------------------- dkdv ----
 
-// Workgroup kj for window key tile kj = ((pos*B + b)*H + h)*NT + t; ROLE 0
-// accumulates dV, ROLE 1 dK (two launches, so that each is compiled for its
-// own register budget).  Lane ln of wave w holds key
-// 32w + swap23(ln): then the V operand read transposed from the pool's V^T
-// tile (whose columns hold the keys in swap23 order) lands in natural lane
-// order.
-template <int ROLE>
-__global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdArgs a) {
-  __shared__ uint4 sQ[kT * 16], sO[kT * 16];    // Q and dO rows of one query tile (64 KB)
-  __shared__ float sLD[2 * kT];                  // LSE*log2(e), then delta
+// One workgroup per window key tile kj = ((pos*B + b)*H + h)*NT + t, eight
+// waves: wave w < 4 (group 0) and wave w + 4 (group 1) share keys
+// 32w + swap23(ln) (lane ln), so that the V operand read transposed from the
+// pool's V^T tile (whose columns hold the keys in swap23 order) lands in
+// natural lane order.  Per 32-query block, group 0 computes S = Q K^T and P,
+// hands P (bf16, already in the B-operand layout) to its partner through LDS
+// and accumulates dV^T += dO^T P; group 1 computes dP = dO V^T meanwhile, then
+// dS = P (dP - delta) and dK^T += Q^T dS.  Both groups issue the same number
+// of MFMAs and one SIMD runs one wave of each, so each wave's VALU work issues
+// beside the other's products.  The kept query tiles are gathered first (mask
+// bits); their Q and dO rows are double-buffered in LDS.  P moves in halves of
+// two blocks (16 KB), with one meeting when a half is written and one when it
+// has been read.
+constexpr int kDkdvThreads = 512;
+
+__device__ inline uint32_t copy_offset8(int wave, int lane) {
+  const int r = 4 * wave + (lane >> 4);
+  return uint32_t(r * 256 + swz_perm((lane & 15) ^ swz_f(r & 15)) * 16);
+}
+// eight waves: copy i of wave w fills LDS chunks [64*(8i + w), +64), rows 32i + 4w + lane/16
+__device__ inline void copy_tile8(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16(src + i * 8192, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 8192u);
+}
+
+__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
+  __shared__ uint4 sQ[2][kT * 16], sO[2][kT * 16];   // Q and dO rows, two query tiles (128 KB)
+  __shared__ uint4 sP[4 * 2 * 2 * 64];               // P operands: [wave pair][block of the half][kk][lane]
+  __shared__ float sLD[2][2 * kT];                   // LSE*log2(e), then delta, per buffer
   __shared__ uint16_t sList[kBwdMaxQTiles];
   __shared__ int sN;
 
-  constexpr int role = ROLE;
   const int kj = blockIdx.x;
   const int t = kj % a.NT;
   const int posbh = kj / a.NT;
@@ -168,23 +186,25 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdArgs a) {
   const int h = bh % a.H, b = bh / a.H;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2, kw = wave & 3;
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
-  const uint32_t voff = copy_offset(wave, lane);
+  const uint32_t voff = copy_offset8(wave, lane);
   const int kvalid = tile_valid(a.tv, t, a.NT, a.tail, kT);
-  const int key = wave * 32 + swap23(ln);       // this lane's key (result column)
+  const int key = kw * 32 + swap23(ln);         // this lane's key (result column)
   const bool key_ok = key < kvalid;
   const int j = pos * a.NT + t;                 // logical key tile
-  const lds_u8* lq = (const lds_u8*)sQ;
-  const lds_u8* lo = (const lds_u8*)sO;
+  const uint8_t* qbase = a.work + size_t(bh) * a.NT * kBwdQTile;
 
-  // the wave's 32 keys as B operands: K rows straight from the page; V rows
-  // (dK only) through LDS, read transposed from the page's V^T
+  // B operands of the wave's keys: group 0 K rows from the page, group 1 V
+  // read transposed from the page's V^T staged in the second dO buffer
   const uint8_t* page = a.pool + ((size_t(a.slot_of[pos]) * a.B * a.H + bh) * a.NT + t) * page_bytes(kT, kD);
-  bf16x8 kf[8], vf[8];
+  bf16x8 bop[8];
+  if (grp == 0) {
 #pragma unroll
-  for (int ks = 0; ks < 8; ++ks)
-    kf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + size_t(key) * 256 + (2 * ks + hl) * 16));
-  if constexpr (role == 1) copy_tile(page + kTile, lds_addr(sO), voff, wave);
+    for (int ks = 0; ks < 8; ++ks)
+      bop[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + size_t(key) * 256 + (2 * ks + hl) * 16));
+  }
+  copy_tile8(page + kTile, lds_addr(&sO[1][0]), voff, wave);
 
   // kept query tiles, ascending
   if (wave == 0) {
@@ -208,98 +228,119 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdArgs a) {
   }
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();
-  if constexpr (role == 1) {
-    // V^T tile row = dim (k-slot 16ks + kappa), columns = key columns 32w ..
+  if (grp == 1) {
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) vf[ks] = tr_operand(lo, wave * 32, lane, [&](int kap) { return 16 * ks + kap; });
+    for (int ks = 0; ks < 8; ++ks)
+      bop[ks] = tr_operand((const lds_u8*)&sO[1][0], kw * 32, lane, [&](int kap) { return 16 * ks + kap; });
   }
   const int N = __builtin_amdgcn_readfirstlane(sN);
+  __syncthreads();                              // V^T consumed: the second buffer is free
 
-  f32x16 acc[4];                                // dV^T or dK^T: [4 dim blocks][32 dims x 32 keys]
+  auto record = [&](int n) { return qbase + size_t(__builtin_amdgcn_readfirstlane(int(sList[n]))) * kBwdQTile; };
+  auto issue = [&](int n) {
+    const uint8_t* rec = record(n);
+    copy_tile8(rec, lds_addr(&sQ[n & 1][0]), voff, wave);
+    copy_tile8(rec + kTile, lds_addr(&sO[n & 1][0]), voff, wave);
+    if (wave == 0) dma16(rec + 2 * kTile, uint32_t(lane) * 16u, lds_addr(&sLD[n & 1][0]));
+  };
+
+  f32x16 acc[4];                                // dV^T (group 0) or dK^T (group 1): [dim block][32 dims x 32 keys]
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x16{};
   const float c2 = a.scale_log2;
-  const uint8_t* qbase = a.work + size_t(bh) * a.NT * kBwdQTile;
+  uint4* pslot = &sP[(kw * 2 * 2) * 64];        // this wave pair's P operands
 
-  // S = Q K^T for 32 queries x the wave's 32 keys
-  auto scores = [&](int qb) {
-    f32x16 sv = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8((const uint8_t*)sQ, swz_elem(qb * 32 + ln, 16 * ks + 8 * hl)),
-                                                   kf[ks], sv, 0, 0, 0);
-    return sv;
-  };
-  // acc^T += X^T op over the block's 32 queries: X (Q or dO rows) read transposed,
-  // k-slot kappa of step kk = query qb*32 + 16kk + swap23(kappa)
-  auto accumulate = [&](const lds_u8* x, int qb, const bf16x8 (&op)[2]) {
+  // acc^T += X^T op over 32 queries: X (Q or dO rows) read transposed, k-slot
+  // kappa of step kk = query qb*32 + 16kk + swap23(kappa).  `lv` is the lane
+  // index made opaque inside the loop, so that the operand addresses are
+  // formed where they are used instead of being held across the loop for both
+  // groups.
+  auto accumulate = [&](const lds_u8* x, int qb, const bf16x8 (&op)[2], int lv) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
         acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            tr_operand(x, mb * 32, lane, [&](int kap) { return qb * 32 + 16 * kk + swap23(kap); }), op[kk], acc[mb],
+            tr_operand(x, mb * 32, lv, [&](int kap) { return qb * 32 + 16 * kk + swap23(kap); }), op[kk], acc[mb],
             0, 0, 0);
   };
+  // X K^T (group 0: S from Q rows) or X V^T (group 1: dP from dO rows) for 32 queries
+  auto product = [&](const uint8_t* x, int qb, int lv) {
+    f32x16 v = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      v = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(x, swz_elem(qb * 32 + (lv & 31), 16 * ks + 8 * (lv >> 5))),
+                                                  bop[ks], v, 0, 0, 0);
+    return v;
+  };
 
+  if (N > 0) issue(0);
   for (int n = 0; n < N; ++n) {
-    const uint8_t* rec = qbase + size_t(__builtin_amdgcn_readfirstlane(int(sList[n]))) * kBwdQTile;
-    __syncthreads();                            // previous tile consumed
-    copy_tile(rec, lds_addr(sQ), voff, wave);
-    copy_tile(rec + kTile, lds_addr(sO), voff, wave);
-    if (wave == 0) dma16(rec + 2 * kTile, uint32_t(lane) * 16u, lds_addr(sLD));
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
-    __syncthreads();
-    if constexpr (role == 0) {
+    __syncthreads();                            // tile n in LDS; tile n-1 fully consumed
+    if (n + 1 < N) issue(n + 1);
+    const uint8_t* lq = reinterpret_cast<const uint8_t*>(&sQ[n & 1][0]);
+    const uint8_t* lo = reinterpret_cast<const uint8_t*>(&sO[n & 1][0]);
+    const float* ld = &sLD[n & 1][0];
 #pragma unroll 1
-      for (int qb = 0; qb < 4; ++qb) {
-        const f32x16 sv = scores(qb);
-        // P; result row r holds query qb*32 + 8*(r/4) + 4*hl + r%4
-        f32x16 p;
+    for (int half = 0; half < 2; ++half) {
+      int lv = lane;
+      asm volatile("" : "+v"(lv));
+      if (grp == 0) {
+        bf16x8 op[2][2];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const float4 l4 = *reinterpret_cast<const float4*>(&sLD[qb * 32 + 8 * g + 4 * hl]);
-          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        for (int u = 0; u < 2; ++u) {
+          const int qb = 2 * half + u;
+          const f32x16 sv = product(lq, qb, lv);
+          // P; result row r holds query qb*32 + 8*(r/4) + 4*hl + r%4
+          f32x16 p;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float w = __builtin_amdgcn_exp2f(sv[4 * g + e] * c2 - lv[e]);
-            p[4 * g + e] = key_ok ? w : 0.f;
+          for (int g = 0; g < 4; ++g) {
+            const float4 l4 = *reinterpret_cast<const float4*>(&ld[qb * 32 + 8 * g + 4 * hl]);
+            const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float w = __builtin_amdgcn_exp2f(sv[4 * g + e] * c2 - lv[e]);
+              p[4 * g + e] = key_ok ? w : 0.f;
+            }
+          }
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            op[u][kk] = rows_to_operand(p, kk);
+            pslot[(u * 2 + kk) * 64 + lane] = __builtin_bit_cast(uint4, op[u][kk]);
           }
         }
-        const bf16x8 op[2] = {rows_to_operand(p, 0), rows_to_operand(p, 1)};
-        __builtin_amdgcn_sched_barrier(0);       // bound the operand reads in flight
-        accumulate(lo, qb, op);                  // dV^T += dO^T P
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    } else {
-#pragma unroll 1
-      for (int qb = 0; qb < 4; ++qb) {
-        const f32x16 sv = scores(qb);
-        __builtin_amdgcn_sched_barrier(0);       // bound the operand reads in flight
-        f32x16 dpv = f32x16{};
+        __syncthreads();                        // P of the half in LDS
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks)
-          dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              lds8((const uint8_t*)sO, swz_elem(qb * 32 + ln, 16 * ks + 8 * hl)), vf[ks], dpv, 0, 0, 0);
-        f32x16 ds;
+        for (int u = 0; u < 2; ++u) accumulate((const lds_u8*)lo, 2 * half + u, op[u], lv);   // dV^T += dO^T P
+      } else {
+        f32x16 dpv[2];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int q0 = qb * 32 + 8 * g + 4 * hl;
-          const float4 l4 = *reinterpret_cast<const float4*>(&sLD[q0]);
-          const float4 d4 = *reinterpret_cast<const float4*>(&sLD[kT + q0]);
-          const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv[4] = {d4.x, d4.y, d4.z, d4.w};
+        for (int u = 0; u < 2; ++u) dpv[u] = product(lo, 2 * half + u, lv);
+        __syncthreads();                        // P of the half in LDS
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * g + e;
-            const float w = __builtin_amdgcn_exp2f(sv[r] * c2 - lv[e]);
-            ds[r] = (key_ok ? w : 0.f) * (dpv[r] - dv[e]);
+        for (int u = 0; u < 2; ++u) {
+          const int qb = 2 * half + u;
+          f32x16 ds;
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            // k-slot e of operand kk is result register 8kk + e
+            const bf16x8 pk = __builtin_bit_cast(bf16x8, pslot[(u * 2 + kk) * 64 + lane]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ds[8 * kk + e] = float(pk[e]);
           }
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const float4 d4 = *reinterpret_cast<const float4*>(&ld[kT + qb * 32 + 8 * g + 4 * hl]);
+            const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ds[4 * g + e] *= dpv[u][4 * g + e] - dv[e];
+          }
+          const bf16x8 op[2] = {rows_to_operand(ds, 0), rows_to_operand(ds, 1)};
+          accumulate((const lds_u8*)lq, qb, op, lv);   // dK^T += Q^T dS
         }
-        const bf16x8 op[2] = {rows_to_operand(ds, 0), rows_to_operand(ds, 1)};
-        __builtin_amdgcn_sched_barrier(0);
-        accumulate(lq, qb, op);                  // dK^T += Q^T dS
-        __builtin_amdgcn_sched_barrier(0);
       }
+      __syncthreads();                          // P of the half consumed
     }
   }
 
@@ -307,8 +348,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdArgs a) {
   // rows inside the chunk (block order) get the zeros they accumulated
   const size_t tok = size_t(t) * kT + key;
   if (tok < size_t(a.L)) {
-    float* dst = (role ? a.dk : a.dv) + (((size_t(pos) * a.B + b) * a.L + tok) * a.H + h) * kD;
-    const float f = role ? a.scale : 1.0f;
+    float* dst = (grp ? a.dk : a.dv) + (((size_t(pos) * a.B + b) * a.L + tok) * a.H + h) * kD;
+    const float f = grp ? a.scale : 1.0f;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -430,9 +471,7 @@ hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream) {
   bwd_prep_kernel<<<qrows, kThreads, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  bwd_dkdv_kernel<1><<<ktiles, kThreads, 0, stream>>>(a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  bwd_dkdv_kernel<0><<<ktiles, kThreads, 0, stream>>>(a);
+  bwd_dkdv_kernel<<<ktiles, kDkdvThreads, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   bwd_dq_kernel<<<qrows, kThreads, 0, stream>>>(a);
   return hipGetLastError();

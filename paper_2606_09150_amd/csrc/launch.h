@@ -101,7 +101,7 @@ struct AttnArgs {
 // the Q and dO rows (zero past the chunk end), then LSE*log2(e) and
 // delta = <dO, O> per query.
 constexpr size_t kBwdQTile = 2 * 32768 + 1024;
-constexpr int kBwdMaxQTiles = 4096;   // query tiles per chunk the backward handles
+constexpr int kBwdMaxQTiles = 2048;   // query tiles per chunk the backward handles
 struct BwdArgs {
   const uint16_t* q;      // [B, L, H, D]
   const uint16_t* o;      // [B, L, H, D]

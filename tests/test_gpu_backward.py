@@ -3,9 +3,9 @@ oracle on the same seeded inputs.
 
 Bar: per (tensor, b, h), ||g_gpu - g_ref||_F / ||g_ref||_F <= 1e-2 for dQ,
 dK and dV.  Derivation: Q, K, V and dO are bf16 inputs, exact on both sides;
-the kernels round P and dS to bf16 (relative 2^-9) before the products that
-give dV, dK and dQ, and take delta from the bf16 forward output, all with fp32
-accumulation.  The rounding errors are independent across terms, so the
+the kernels round P and dS to bf16 (relative 2^-9 each; dS is formed from the
+bf16 P) before the products that give dV, dK and dQ, and take delta from the
+bf16 forward output, all with fp32 accumulation.  The rounding errors are independent across terms, so the
 normwise error stays a small multiple of 2^-9 = 2.0e-3; 1e-2 leaves that
 margin and equals the forward's bar.  Keys that no row keeps must get exactly
 zero.  Full comparison at sizes the oracle finishes in seconds (ragged tails,
