@@ -28,6 +28,7 @@
 #include <type_traits>
 
 #include "attn_common.h"
+#include "../launch_bwd.h"
 
 namespace uf {
 namespace {

@@ -18,6 +18,7 @@
 #include <vector>
 
 #include "launch.h"
+#include "launch_bwd.h"
 
 namespace {
 
