@@ -9,7 +9,8 @@
 //
 // Three kernels, all with 32x32x16 bf16 MFMA and fp32 accumulation:
 //  * prep: per query tile, Q and dO rows (rows past the chunk end zero),
-//    LSE*log2(e) (+inf on those rows, so that their weights vanish) and delta;
+//    -LSE/scale (-inf on those rows, so that their weights vanish) and
+//    -delta, which seed the S and dP accumulators;
 //  * dkdv: per window key tile, one workgroup accumulating dK and (a second
 //    launch) one accumulating dV, four waves of 32 keys each; they walk the query tiles whose lists keep
 //    the tile (mask bits) and per 32-query block compute S = Q K^T (keys on the
@@ -67,20 +68,20 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(BwdArgs a) {
     qr[c] = vq;
     orow[c] = vo;
   }
-  float* lse2 = reinterpret_cast<float*>(rec + 2 * kTile);
-  float* delta = lse2 + kT;
+  float* nlse = reinterpret_cast<float*>(rec + 2 * kTile);
+  float* ndelta = nlse + kT;
   if (threadIdx.x < kT) {
     const int q = threadIdx.x;
-    float l2 = INFINITY, dl = 0.f;
+    float nl = -INFINITY, dl = 0.f;
     if (q < nv) {
       const size_t tok = size_t(i) * kT + q;
-      l2 = a.lse[(size_t(b) * a.H + h) * a.L + tok] * 1.4426950408889634f;
+      nl = -a.lse[(size_t(b) * a.H + h) * a.L + tok] / a.scale;
       const uint16_t* op = a.o + ((size_t(b) * a.L + tok) * a.H + h) * kD;
       const uint16_t* gp = a.dout + ((size_t(b) * a.L + tok) * a.H + h) * kD;
       for (int d = 0; d < kD; ++d) dl += bf16f(op[d]) * bf16f(gp[d]);
     }
-    lse2[q] = l2;
-    delta[q] = dl;
+    nlse[q] = nl;
+    ndelta[q] = -dl;
   }
 }
 
@@ -145,6 +146,54 @@ __device__ inline bf16x8 rows_to_operand(const f32x16& x, int kk) {
   return r;
 }
 
+// Per-lane parts of operand addresses, computed once per kernel so that every
+// read in the loops is a fixed register plus a compile-time offset.
+//
+// TrTable: transposing reads from a k-major tile whose k-slot kappa of a
+// 16-row step starting at row R (a multiple of 16) is row R + kappa
+// (natural) or R + swap23(kappa) (SWAP); t[h][cb] is the byte offset, minus
+// R*256, of read h of the operand over columns 32*cb .. 32*cb + 31.
+struct TrTable {
+  uint32_t t[2][4];
+};
+template <bool SWAP>
+__device__ inline TrTable tr_table(int lane) {
+  const int rp = lane & 15, g = (lane >> 4) & 1, hl = lane >> 5;
+  TrTable T;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int lrow = SWAP ? 8 * h + 4 * hl + (rp >> 2) : 8 * hl + 4 * h + (rp >> 2);
+      T.t[h][cb] = swz_elem(lrow, 32 * cb + 16 * g + 4 * (rp & 3));
+    }
+  return T;
+}
+__device__ inline bf16x8 tr_op(const lds_u8* tile, const TrTable& T, int R, int cb) {
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(tile + R * 256 + T.t[0][cb]));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(tile + R * 256 + T.t[1][cb]));
+  const v4i16 v[2] = {lo, hi};
+  return __builtin_bit_cast(bf16x8, v);
+}
+// RowTable: 16-byte row reads of an A/B operand (lane holds row R + rl, rl = ln
+// or swap23(ln), R a multiple of 32; dims 16ks + 8hl .. +7): u[ks] is the
+// byte offset minus R*256.
+struct RowTable {
+  uint32_t u[8];
+};
+template <bool SWAP>
+__device__ inline RowTable row_table(int lane) {
+  const int ln = lane & 31, hl = lane >> 5;
+  const int rl = SWAP ? swap23(ln) : ln;
+  RowTable U;
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) U.u[ks] = swz_elem(rl, 16 * ks + 8 * hl);
+  return U;
+}
+__device__ inline bf16x8 row_op(const uint8_t* tile, const RowTable& U, int R, int ks) {
+  return lds8(tile, uint32_t(R * 256) + U.u[ks]);
+}
+
 // ---------------------------------------------------------------- dkdv ----
 
 // One workgroup per window key tile kj = ((pos*B + b)*H + h)*NT + t, eight
@@ -153,13 +202,12 @@ __device__ inline bf16x8 rows_to_operand(const f32x16& x, int kk) {
 // pool's V^T tile (whose columns hold the keys in swap23 order) lands in
 // natural lane order.  Per 32-query block, group 0 computes S = Q K^T and P,
 // hands P (bf16, already in the B-operand layout) to its partner through LDS
-// and accumulates dV^T += dO^T P; group 1 computes dP = dO V^T meanwhile, then
-// dS = P (dP - delta) and dK^T += Q^T dS.  Both groups issue the same number
-// of MFMAs and one SIMD runs one wave of each, so each wave's VALU work issues
-// beside the other's products.  The kept query tiles are gathered first (mask
-// bits); their Q and dO rows are double-buffered in LDS.  P moves in halves of
-// two blocks (16 KB), with one meeting when a half is written and one when it
-// has been read.
+// and accumulates dV^T += dO^T P; group 1 computes dP = dO V^T, then
+// dS = P (dP - delta) and dK^T += Q^T dS.  The S and dP accumulators start
+// from the workspace's -LSE/scale and -delta, so P = exp2(c2 S') and
+// dS = P dP' need no subtraction.  Both groups issue the same number of MFMAs
+// and one SIMD runs one wave of each.  The kept query tiles are gathered first
+// (mask bits); their Q and dO rows are double-buffered in LDS.
 constexpr int kDkdvThreads = 512;
 
 __device__ inline uint32_t copy_offset8(int wave, int lane) {
@@ -175,7 +223,7 @@ __device__ inline void copy_tile8(const uint8_t* src, uint32_t lds_tile, uint32_
 __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   __shared__ uint4 sQ[2][kT * 16], sO[2][kT * 16];   // Q and dO rows, two query tiles (128 KB)
   __shared__ uint4 sP[4 * 2 * 2 * 64];               // P operands: [wave pair][block of the half][kk][lane]
-  __shared__ float sLD[2][2 * kT];                   // LSE*log2(e), then delta, per buffer
+  __shared__ float sLD[2][2 * kT];                   // -LSE/scale, then -delta, per buffer
   __shared__ uint16_t sList[kBwdMaxQTiles];
   __shared__ int sN;
 
@@ -250,100 +298,109 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x16{};
   const float c2 = a.scale_log2;
   uint4* pslot = &sP[(kw * 2 * 2) * 64];        // this wave pair's P operands
+  const TrTable TT = tr_table<true>(lane);      // X^T reads: k-slot kappa = query 16kk + swap23(kappa)
+  const RowTable RT = row_table<false>(lane);   // X rows: query qb*32 + ln
 
-  // acc^T += X^T op over 32 queries: X (Q or dO rows) read transposed, k-slot
-  // kappa of step kk = query qb*32 + 16kk + swap23(kappa).  `lv` is the lane
-  // index made opaque inside the loop, so that the operand addresses are
-  // formed where they are used instead of being held across the loop for both
-  // groups.
-  auto accumulate = [&](const lds_u8* x, int qb, const bf16x8 (&op)[2], int lv) {
+  // acc^T += X^T op over the block's 32 queries (X = Q or dO rows, read transposed)
+  auto accumulate = [&](const lds_u8* x, int qb, const bf16x8 (&op)[2]) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            tr_operand(x, mb * 32, lv, [&](int kap) { return qb * 32 + 16 * kk + swap23(kap); }), op[kk], acc[mb],
-            0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_op(x, TT, qb * 32 + 16 * kk, mb), op[kk], acc[mb], 0, 0, 0);
   };
-  // X K^T (group 0: S from Q rows) or X V^T (group 1: dP from dO rows) for 32 queries
-  auto product = [&](const uint8_t* x, int qb, int lv) {
-    f32x16 v = f32x16{};
+  // c0 + X K^T (group 0: S - LSE/scale from Q rows) or c0 + X V^T (group 1:
+  // dP - delta from dO rows) for 32 queries; c0 holds the per-query term in
+  // the result layout (register 4g + e = query qb*32 + 8g + 4hl + e), read
+  // from the workspace's per-query values.
+  auto product = [&](const uint8_t* x, const float* c, int qb) {
+    f32x16 v;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 c4 = *reinterpret_cast<const float4*>(&c[qb * 32 + 8 * g + 4 * hl]);
+      v[4 * g] = c4.x;
+      v[4 * g + 1] = c4.y;
+      v[4 * g + 2] = c4.z;
+      v[4 * g + 3] = c4.w;
+    }
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      v = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds8(x, swz_elem(qb * 32 + (lv & 31), 16 * ks + 8 * (lv >> 5))),
-                                                  bop[ks], v, 0, 0, 0);
+      v = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_op(x, RT, qb * 32, ks), bop[ks], v, 0, 0, 0);
     return v;
   };
+  // group 0, block qb: S, P (as bf16 B operands, also written to the block's P slot)
+  auto scores = [&](const uint8_t* lq, const float* ld, int qb, bf16x8 (&op)[2]) {
+    const f32x16 sv = product(lq, ld, qb);      // S - LSE/scale (-inf on padding queries)
+    f32x16 p;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float w = __builtin_amdgcn_exp2f(sv[r] * c2);
+      p[r] = key_ok ? w : 0.f;
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      op[kk] = rows_to_operand(p, kk);
+      pslot[((qb & 1) * 2 + kk) * 64 + lane] = __builtin_bit_cast(uint4, op[kk]);
+    }
+  };
+  // group 1, block qb: dS = P (dP - delta) from the block's P slot, dK^T += Q^T dS
+  auto dk_block = [&](const lds_u8* lq, int qb, const f32x16& dpv) {
+    f32x16 ds;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      // k-slot e of operand kk is result register 8kk + e
+      const bf16x8 pk = __builtin_bit_cast(bf16x8, pslot[((qb & 1) * 2 + kk) * 64 + lane]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ds[8 * kk + e] = float(pk[e]) * dpv[8 * kk + e];
+    }
+    const bf16x8 op[2] = {rows_to_operand(ds, 0), rows_to_operand(ds, 1)};
+    accumulate(lq, qb, op);
+  };
 
-  if (N > 0) issue(0);
-  for (int n = 0; n < N; ++n) {
+  // Per tile, five steps separated by meetings; P slot qb&1 carries block qb
+  // from group 0 (step qb) to group 1 (step qb+1):
+  //   step 0: group 0 S, P of block 0            | group 1 dP of block 0
+  //   step s: group 0 S, P of block s, dV of s-1 | group 1 dS, dK of s-1, dP of s
+  //   step 4: group 0 dV of block 3              | group 1 dS, dK of block 3
+  // so that in the three middle steps both waves of a SIMD have 16 MFMAs.
+  // The buffer of tile n is n&1; the loop runs two tiles per trip so that the
+  // buffer, and with it every operand address, is a compile-time offset.
+  // Each group runs its own copy of the tile loop (same meetings in the same
+  // order), so that no branch on the group sits inside the loop and the
+  // accumulators keep their registers.
+  auto tile = [&](int n, auto buf, auto group) {
+    constexpr int B = decltype(buf)::value;
+    constexpr int G = decltype(group)::value;
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();                            // tile n in LDS; tile n-1 fully consumed
     if (n + 1 < N) issue(n + 1);
-    const uint8_t* lq = reinterpret_cast<const uint8_t*>(&sQ[n & 1][0]);
-    const uint8_t* lo = reinterpret_cast<const uint8_t*>(&sO[n & 1][0]);
-    const float* ld = &sLD[n & 1][0];
-#pragma unroll 1
-    for (int half = 0; half < 2; ++half) {
-      int lv = lane;
-      asm volatile("" : "+v"(lv));
-      if (grp == 0) {
-        bf16x8 op[2][2];
+    const uint8_t* lq = reinterpret_cast<const uint8_t*>(&sQ[B][0]);
+    const uint8_t* lo = reinterpret_cast<const uint8_t*>(&sO[B][0]);
+    const float* ld = &sLD[B][0];
+    bf16x8 op[2][2];                            // group 0: P operands of the last two blocks
+    f32x16 dpv[2];                              // group 1: dP - delta of the last two blocks
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int qb = 2 * half + u;
-          const f32x16 sv = product(lq, qb, lv);
-          // P; result row r holds query qb*32 + 8*(r/4) + 4*hl + r%4
-          f32x16 p;
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const float4 l4 = *reinterpret_cast<const float4*>(&ld[qb * 32 + 8 * g + 4 * hl]);
-            const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float w = __builtin_amdgcn_exp2f(sv[4 * g + e] * c2 - lv[e]);
-              p[4 * g + e] = key_ok ? w : 0.f;
-            }
-          }
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            op[u][kk] = rows_to_operand(p, kk);
-            pslot[(u * 2 + kk) * 64 + lane] = __builtin_bit_cast(uint4, op[u][kk]);
-          }
-        }
-        __syncthreads();                        // P of the half in LDS
-#pragma unroll
-        for (int u = 0; u < 2; ++u) accumulate((const lds_u8*)lo, 2 * half + u, op[u], lv);   // dV^T += dO^T P
+    for (int st = 0; st < 5; ++st) {
+      if constexpr (G == 0) {
+        if (st < 4) scores(lq, ld, st, op[st & 1]);
+        if (st > 0) accumulate((const lds_u8*)lo, st - 1, op[(st - 1) & 1]);   // dV^T += dO^T P
       } else {
-        f32x16 dpv[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) dpv[u] = product(lo, 2 * half + u, lv);
-        __syncthreads();                        // P of the half in LDS
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int qb = 2 * half + u;
-          f32x16 ds;
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            // k-slot e of operand kk is result register 8kk + e
-            const bf16x8 pk = __builtin_bit_cast(bf16x8, pslot[(u * 2 + kk) * 64 + lane]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ds[8 * kk + e] = float(pk[e]);
-          }
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const float4 d4 = *reinterpret_cast<const float4*>(&ld[kT + qb * 32 + 8 * g + 4 * hl]);
-            const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) ds[4 * g + e] *= dpv[u][4 * g + e] - dv[e];
-          }
-          const bf16x8 op[2] = {rows_to_operand(ds, 0), rows_to_operand(ds, 1)};
-          accumulate((const lds_u8*)lq, qb, op, lv);   // dK^T += Q^T dS
-        }
+        if (st > 0) dk_block((const lds_u8*)lq, st - 1, dpv[(st - 1) & 1]);
+        if (st < 4) dpv[st & 1] = product(lo, ld + kT, st);
       }
-      __syncthreads();                          // P of the half consumed
+      if (st < 4) __syncthreads();              // P of block st written; block st-1 consumed
     }
-  }
+  };
+  auto run = [&](auto group) {
+    for (int n = 0; n < N; n += 2) {
+      tile(n, std::integral_constant<int, 0>{}, group);
+      if (n + 1 < N) tile(n + 1, std::integral_constant<int, 1>{}, group);
+    }
+  };
+
+  if (N > 0) issue(0);
+  if (grp == 0) run(std::integral_constant<int, 0>{});
+  else run(std::integral_constant<int, 1>{});
 
   // store: lane holds key `key`, dims mb*32 + 8*(r/4) + 4*hl + r%4; padding
   // rows inside the chunk (block order) get the zeros they accumulated
@@ -389,9 +446,18 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(rec + size_t(q) * 256 + (2 * ks + hl) * 16));
     of[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(rec + kTile + size_t(q) * 256 + (2 * ks + hl) * 16));
   }
-  const float l2 = reinterpret_cast<const float*>(rec + 2 * kTile)[q];
-  const float dl = reinterpret_cast<const float*>(rec + 2 * kTile)[kT + q];
+  // per-lane query terms as MFMA seeds: S^T - LSE/scale and dP^T - delta
+  const float nl = reinterpret_cast<const float*>(rec + 2 * kTile)[q];
+  const float nd = reinterpret_cast<const float*>(rec + 2 * kTile)[kT + q];
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  f32x16 negl, negd;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    negl[r] = nl;
+    negd[r] = nd;
+  }
+  const TrTable TT = tr_table<false>(lane);    // K^T and V reads: k-slot kappa = row R + kappa
+  const RowTable RT = row_table<true>(lane);   // K rows kb*32 + swap23(ln)
 
   f32x16 dqt[4];                                // [4 dim blocks][32 dims x 32 queries]
 #pragma unroll
@@ -417,39 +483,38 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     copy_tile(page + kTile, lds_addr(sV), voff, wave);
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
-#pragma unroll 1
+#pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       // S^T = K Q^T and dP^T = V dO^T: A operands are K rows kb*32 + swap23(ln)
-      // and V read transposed from V^T (tile row = dim, columns kb*32 ..)
-      f32x16 sv = f32x16{}, dpv = f32x16{};
+      // and V read transposed from V^T (tile row = dim, columns kb*32 ..);
+      // keys past the tile's valid rows start at -inf, so their weights vanish
+      f32x16 sv = negl, dpv = negd;
+      if (kvalid < kT) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (kb * 32 + swap23(8 * (r >> 2) + 4 * hl + (r & 3)) >= kvalid) sv[r] = -INFINITY;
+      }
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            lds8((const uint8_t*)sK, swz_elem(kb * 32 + swap23(ln), 16 * ks + 8 * hl)), qf[ks], sv, 0, 0, 0);
-        dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            tr_operand(lv, kb * 32, lane, [&](int kap) { return 16 * ks + kap; }), of[ks], dpv, 0, 0, 0);
+        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_op((const uint8_t*)sK, RT, kb * 32, ks), qf[ks], sv, 0, 0, 0);
+        dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_op(lv, TT, 16 * ks, kb), of[ks], dpv, 0, 0, 0);
       }
       // result row m = 8*(r/4) + 4*hl + r%4 holds key kb*32 + swap23(m)
       f32x16 ds;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kb * 32 + swap23(8 * (r >> 2) + 4 * hl + (r & 3));
-        const float e = __builtin_amdgcn_exp2f(sv[r] * c2 - l2);
-        ds[r] = (key < kvalid ? e : 0.f) * (dpv[r] - dl);
-      }
+      for (int r = 0; r < 16; ++r) ds[r] = __builtin_amdgcn_exp2f(sv[r] * c2) * dpv[r];
       // dQ^T += K^T dS^T: k-slot kappa of step kk = key kb*32 + 16kk + kappa
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         const bf16x8 db = rows_to_operand(ds, kk);
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
-          dqt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              tr_operand(lk, mb * 32, lane, [&](int kap) { return kb * 32 + 16 * kk + kap; }), db, dqt[mb], 0, 0, 0);
+          dqt[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_op(lk, TT, kb * 32 + 16 * kk, mb), db, dqt[mb], 0, 0, 0);
       }
     }
   }
 
-  // padding rows inside the chunk accumulated zeros (their LSE is +inf)
+  // padding rows inside the chunk accumulated zeros (their seed is -inf)
   if (size_t(i) * kT + q < size_t(a.L)) {
     const size_t base = ((size_t(b) * a.L + size_t(i) * kT + q) * a.H + h) * kD;
 #pragma unroll

@@ -6,8 +6,8 @@
 namespace uf {
 
 // Backward of the attention.  The workspace holds, per query tile (b, h, i),
-// the Q and dO rows (zero past the chunk end), then LSE*log2(e) and
-// delta = <dO, O> per query.
+// the Q and dO rows (zero past the chunk end), then -LSE/scale (-inf past the
+// chunk end) and -delta = -<dO, O> per query.
 constexpr size_t kBwdQTile = 2 * 32768 + 1024;
 constexpr int kBwdMaxQTiles = 2048;   // query tiles per chunk the backward handles
 struct BwdArgs {
