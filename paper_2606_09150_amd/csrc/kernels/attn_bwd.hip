@@ -333,9 +333,10 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     const f32x16 sv = product(lq, ld, qb);      // S - LSE/scale (-inf on padding queries)
     f32x16 p;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float w = __builtin_amdgcn_exp2f(sv[r] * c2);
-      p[r] = key_ok ? w : 0.f;
+    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(sv[r] * c2);
+    if (kvalid < kT) {                          // padding keys (lanes) weigh nothing
+#pragma unroll
+      for (int r = 0; r < 16; ++r) p[r] = key_ok ? p[r] : 0.f;
     }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
@@ -487,17 +488,21 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     for (int kb = 0; kb < 4; ++kb) {
       // S^T = K Q^T and dP^T = V dO^T: A operands are K rows kb*32 + swap23(ln)
       // and V read transposed from V^T (tile row = dim, columns kb*32 ..);
-      // keys past the tile's valid rows start at -inf, so their weights vanish
-      f32x16 sv = negl, dpv = negd;
-      if (kvalid < kT) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (kb * 32 + swap23(8 * (r >> 2) + 4 * hl + (r & 3)) >= kvalid) sv[r] = -INFINITY;
-      }
+      f32x16 sv, dpv;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_op((const uint8_t*)sK, RT, kb * 32, ks), qf[ks], sv, 0, 0, 0);
-        dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_op(lv, TT, 16 * ks, kb), of[ks], dpv, 0, 0, 0);
+        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_op((const uint8_t*)sK, RT, kb * 32, ks), qf[ks],
+                                                     ks ? sv : negl, 0, 0, 0);
+        dpv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_op(lv, TT, 16 * ks, kb), of[ks], ks ? dpv : negd, 0, 0, 0);
+      }
+      // keys past the tile's valid rows get -inf, so their weights vanish (a
+      // rare case: the key indices are formed here, not held across the loop)
+      if (kvalid < kT) {
+        int h4 = 4 * hl;
+        asm volatile("" : "+v"(h4));
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (kb * 32 + swap23(8 * (r >> 2) + h4 + (r & 3)) >= kvalid) sv[r] = -INFINITY;
       }
       // result row m = 8*(r/4) + 4*hl + r%4 holds key kb*32 + swap23(m)
       f32x16 ds;
