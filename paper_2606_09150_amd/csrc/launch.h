@@ -25,10 +25,14 @@ struct TileValid {
   int32_t blocked;                 // 0: raster tiles
   int32_t nbh, nbw;                // block rows and columns of the grid (blocked)
   int32_t local_half;              // M_local half-width in blocks, -1: no local mask
-  uint8_t count[UF_MAX_BLOCKS];    // valid rows of tile t (blocked)
+  // valid rows of tile t (blocked): byte t % 4 of word t / 4, so that a
+  // uniform index reads the kernel arguments with one scalar load (a byte
+  // read would be a vector load, and the wait for it a wait for every copy
+  // in flight)
+  uint32_t count4[UF_MAX_BLOCKS / 4];
 };
 __host__ __device__ inline int tile_valid(const TileValid& v, int t, int NT, int tail, int T) {
-  return v.blocked ? int(v.count[t]) : ((t == NT - 1) ? tail : T);
+  return v.blocked ? int((v.count4[t >> 2] >> (8 * (t & 3))) & 0xffu) : ((t == NT - 1) ? tail : T);
 }
 // M_local between query tile i and key tile t (block indices of one chunk).
 __host__ __device__ inline bool tile_local(const TileValid& v, int i, int t) {

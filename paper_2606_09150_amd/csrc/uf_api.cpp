@@ -82,7 +82,8 @@ struct uf_kv {
     v.nbh = blocked ? nbh : 1;
     v.nbw = blocked ? nbw : 1;
     v.local_half = (blocked && local_r > 0) ? local_r / 2 : -1;
-    if (blocked) std::memcpy(v.count, block_valid, sizeof(block_valid));
+    if (blocked)
+      for (int32_t j = 0; j < UF_MAX_BLOCKS; ++j) v.count4[j >> 2] |= uint32_t(block_valid[j]) << (8 * (j & 3));
     return v;
   }
   // pooled keys follow the pages: [max_chunks][B][H][NT][D] float32
