@@ -69,7 +69,7 @@ def measured_traffic(config):
         if fields["workload"] != config or fields["kernel_sources_sha256"] != attn_sources_sha256():
             return None
         return int(fields["traffic_bytes_per_launch"])
-    except (KeyError, ValueError):
+    except (KeyError, ValueError, OSError):
         return None
 
 
