@@ -167,3 +167,45 @@ def test_backward_1k_sampled_rows_and_identities():
         tv = (gv[:, 0, :, h] * vs[:, :, h]).sum(-1)
         to = (hdo[0, :, h] * go[0, :, h]).sum(-1)
         assert abs(tv.sum() - to.sum()) <= GRAD_TOL * (np.abs(tv).sum() + np.abs(to).sum())
+
+
+def test_backward_empty_rows_and_stale_entries():
+    """A row with no kept tile gets zero gradients and gives none; a list entry
+    outside the window counts no key (hand-made lists, index and mask sections
+    kept consistent)."""
+    P = require_gpu()
+    log("bwd empty rows + stale entries")
+    case = Case(P, 1, 300, 2, 128, 4, True, seed=2103)
+    for _ in range(3):
+        case.append()
+    counts, idx, mask = case.gpu_lists(case.rule(1.0))
+    nt, nk = 3, 9
+    counts, idx, mask = counts.copy(), idx.copy(), mask.copy()
+    counts[0, 0, 1] = 0                          # empty row
+    idx[0, 0, 1, :] = -1
+    mask[0, 0, 1, :] = 0
+    idx[0, 1, 2, :] = -1                         # row keeps tiles 0, 4 and a stale 50
+    idx[0, 1, 2, :3] = [0, 4, 50]
+    counts[0, 1, 2] = 3
+    mask[0, 1, 2, :] = 0
+    mask[0, 1, 2, 0] = (1 << 0) | (1 << 4)
+    c_v, i_v, m_v = case.win.lists_views()
+    c_v.copy_(torch.from_numpy(counts))
+    i_v.copy_(torch.from_numpy(idx))
+    m_v.copy_(torch.from_numpy(mask.view(np.int32)))
+    scale = 1 / math.sqrt(128)
+    q = case.query()
+    o, lse = case.win.attention(q, scale)
+    do = case._draw(case.n_appended - 1, "do")
+    dq, dk, dv = case.win.attention_bwd(q, o, lse, do, scale)
+    torch.cuda.synchronize()
+    bits = np.ones((1, 2, nt, nk), dtype=bool)
+    bits[0, 0, 1] = False
+    bits[0, 1, 2] = False
+    bits[0, 1, 2, [0, 4]] = True
+    rq, rk, rv = oracle.sparse_causal_attention_bwd(case.ring, case._host(q), case._host(do), bits, 128, scale)
+    gq, gk, gv = dq.cpu().numpy(), dk.cpu().numpy(), dv.cpu().numpy()
+    assert np.all(gq[0, 128:256, 0] == 0)
+    for h in range(2):
+        for g, r in ((gq[0, :, h], rq[0, :, h]), (gk[:, 0, :, h], rk[:, 0, :, h]), (gv[:, 0, :, h], rv[:, 0, :, h])):
+            assert _normwise(g, r) <= GRAD_TOL
