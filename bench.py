@@ -150,6 +150,7 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
         "ms_per_step": ms_step,
         "value": kept / (ms_step * 1e-3) / 1e12,
         "attn_ms": attn_avg,
+        "attn_ms_median": attn_sorted[len(attn_sorted) // 2],
         "attn_ms_p10": attn_sorted[len(attn_sorted) // 10],
         "attn_ms_p90": attn_sorted[(9 * len(attn_sorted)) // 10],
         "attn_tflops": kept / (attn_avg * 1e-3) / 1e12,
@@ -343,6 +344,50 @@ def sparsity_sweep(wl, state, sparsities=(0.12, 0.35, 0.58, 0.72, 0.82), reps=10
     return rows
 
 
+def run_stream(P, wl):
+    """The streaming configuration: wl.stream_chunks chunks pushed one by one
+    through the window (evict the oldest non-pinned chunk once it is full,
+    append, build lists, attend), every chunk timed; the steady state is the
+    chunks after the window first fills."""
+    import torch
+    import synth
+
+    dev = torch.device("cuda", 0)
+    B, L, H, T = wl.batch, wl.chunk_tokens, wl.heads, wl.tile
+    nt = -(-L // T)
+    tail = L - (nt - 1) * T
+    win = P.KVWindow(B, H, L, T, wl.max_chunks, wl.pin_sink, device=dev)
+    out = torch.empty((B, L, H, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
+    scale = 1.0 / math.sqrt(D)
+    stream = torch.cuda.current_stream(dev)
+    chunks = []
+    for c in range(wl.stream_chunks):
+        src = {name: synth.chunk_tensor(wl, c, name, device="cuda") for name in ("k", "v", "q")}
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        if win.info().n_live == wl.max_chunks:
+            win.evict(1)
+        win.append(src["k"], src["v"])
+        win.build_lists(wl.seed, wl.p_prior)
+        ev[1].record(stream)
+        win.attention(src["q"], scale, out=out, lse=lse)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        kept, _ = _flops_of_lists(win, win.lists, nt, tail, T)
+        attn = ev[1].elapsed_time(ev[2])
+        chunks.append({"chunk": c, "n_live": win.info().n_live, "path_ms": ev[0].elapsed_time(ev[2]),
+                       "attn_ms": attn, "attn_tflops": kept / (attn * 1e-3) / 1e12})
+    steady = [x for x in chunks if x["chunk"] >= wl.max_chunks - 1]
+    return {"workload": f"{wl.name}: {H} heads, {wl.stream_chunks} chunks through a {wl.max_chunks}-chunk window",
+            "steady_state_chunks": f"{steady[0]['chunk']}..{steady[-1]['chunk']}",
+            "steady_attn_ms": sum(x["attn_ms"] for x in steady) / len(steady),
+            "steady_path_ms": sum(x["path_ms"] for x in steady) / len(steady),
+            "steady_attn_tflops": sum(x["attn_tflops"] for x in steady) / len(steady),
+            "per_chunk": [{k: (round(v, 4) if isinstance(v, float) else v) for k, v in x.items()} for x in chunks]}
+
+
 def cpu_baseline(wl, state, target_s):
     """The oracle, as it stands, on a bounded sample: head 0 of the last window, leading q-tiles."""
     import numpy as np
@@ -392,10 +437,17 @@ def cpu_baseline(wl, state, target_s):
     t0 = time.perf_counter()
     oracle.sparse_causal_attention(ring, q, bits, T, scale, qtiles=tiles)
     sec = time.perf_counter() - t0
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": kept_flops(tiles) / sec / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
+        "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": f"{wl.name}: head 0, query tiles 1..{n} of {nt} ({n * T} queries x {L * info.n_live} keys, "
                   f"float64 numpy masked-dense), {sec:.1f} s; throughput in kept-tile FLOP/s",
@@ -417,6 +469,8 @@ def main():
     ap.add_argument("--blocks", action="store_true",
                     help="also run the workload on (2, 8, 8) blocks with the local window r = 9")
     ap.add_argument("--no-bwd", action="store_true", help="skip timing the backward (dQ, dK, dV)")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the other workloads (480p dense, tiny, the 40-head 1K stream)")
     ap.add_argument("--sweep", action="store_true",
                     help="also time the attention against sparsity (top-k lists, no forced chunks)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -492,6 +546,18 @@ def main():
         res2["roofline_frac"] = res2["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
         line["secondary"] = res2
         del state2
+        torch.cuda.empty_cache()
+    if not args.no_others:
+        others = {}
+        for name in ("480p", "tiny"):
+            r, st2 = run_workload(P, synth.WORKLOADS[name], 10, args.warmup)
+            keep = ("workload", "ms_per_step", "attn_ms", "attn_ms_median", "attn_tflops", "append_us", "append_gbps",
+                    "lists_us", "kept_fraction")
+            others[name] = {k: r[k] for k in keep}
+            others[name]["roofline_frac"] = r["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
+            del st2
+        others["1k_stream"] = run_stream(P, synth.WORKLOADS["1k_stream"])
+        line["others"] = others
         torch.cuda.empty_cache()
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 20
