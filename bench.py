@@ -145,6 +145,8 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     attn_avg = sum(attn_ms) / steps
     attn_sorted = sorted(attn_ms)
     append_bytes = 2 * B * L * H * D * 2 + 2 * B * nt * T * H * D * 2 + B * nt * H * D * 4
+    # unique bytes of one attention launch: Q, the window's K/V pages, O and LSE
+    unique_bytes = B * L * H * D * 2 + wl.window_chunks * B * nt * H * 4 * T * D + B * L * H * D * 2 + B * H * L * 4
     res = {
         "workload": wl.name,
         "ms_per_step": ms_step,
@@ -158,6 +160,7 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
         "append_gbps": append_bytes / (sum(append_ms) / steps * 1e-3) / 1e9,
         "lists_us": sum(lists_ms) / steps * 1e3,
         "kept_tflop_per_step": kept / 1e12,
+        "attn_unique_gbps": unique_bytes / (attn_avg * 1e-3) / 1e9,
         "kept_fraction": kept / dense,
         "padded_tile_tflop_per_step": padded / 1e12,
         "keys": L * wl.window_chunks,
@@ -551,8 +554,8 @@ def main():
         others = {}
         for name in ("480p", "tiny"):
             r, st2 = run_workload(P, synth.WORKLOADS[name], 10, args.warmup)
-            keep = ("workload", "ms_per_step", "attn_ms", "attn_ms_median", "attn_tflops", "append_us", "append_gbps",
-                    "lists_us", "kept_fraction")
+            keep = ("workload", "ms_per_step", "attn_ms", "attn_ms_median", "attn_tflops", "attn_unique_gbps",
+                    "append_us", "append_gbps", "lists_us", "kept_fraction")
             others[name] = {k: r[k] for k in keep}
             others[name]["roofline_frac"] = r["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
             del st2
