@@ -223,6 +223,7 @@ def run_backward(P, wl, state, reps=10, warmup=2):
     ms = ev[0].elapsed_time(ev[1]) / reps
     flops = state["kept_flops"] * 10 // 4
     return {"bwd_ms": ms, "bwd_tflop": flops / 1e12, "bwd_tflops": flops / (ms * 1e-3) / 1e12,
+            "bwd_roofline_frac": flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
             "bwd_work_bytes": work.numel(), "bwd_reps": reps}
 
 
@@ -547,6 +548,8 @@ def main():
         wl2 = synth.WORKLOADS[args.secondary]
         res2, state2 = run_workload(P, wl2, max(5, args.steps // 2), args.warmup)
         res2["roofline_frac"] = res2["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
+        if not args.no_bwd:
+            res2["backward"] = run_backward(P, wl2, state2)
         line["secondary"] = res2
         del state2
         torch.cuda.empty_cache()

@@ -10,9 +10,9 @@ normwise error stays a small multiple of 2^-9 = 2.0e-3; 1e-2 leaves that
 margin and equals the forward's bar.  Keys that no row keeps must get exactly
 zero.  Full comparison at sizes the oracle finishes in seconds (ragged tails,
 batch 2, evictions, a one-token chunk) and on two heads of the 480p window;
-at the 1K window (the launch that bench.py times) sampled dQ rows against the
-oracle and, on every head, identities that the exact gradients satisfy at any
-size.
+at the 1K and 2K windows (the launches that bench.py times) sampled dQ rows
+against the oracle and, on every head, identities that the exact gradients
+satisfy at any size.
 """
 
 import math
@@ -130,10 +130,11 @@ def test_backward_480p_full_two_heads():
     _full_compare(case, case.rule(wl.p_prior), heads=[0, 7])
 
 
-def test_backward_1k_sampled_rows_and_identities():
+@pytest.mark.parametrize("name", ["1k", "2k"])
+def test_backward_sampled_rows_and_identities(name):
     P = require_gpu()
-    wl = synth.WORKLOADS["1k"]
-    log("bwd workload=1k sampled + identities")
+    wl = synth.WORKLOADS[name]
+    log(f"bwd workload={name} sampled + identities")
     case = Case(P, 1, wl.chunk_tokens, wl.heads, wl.tile, wl.max_chunks, wl.pin_sink, wl.seed, gen_device="cuda")
     for _ in range(wl.window_chunks):
         case.append()
