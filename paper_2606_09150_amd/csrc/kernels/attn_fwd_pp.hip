@@ -513,6 +513,11 @@ hipError_t launch_attn_fwd_t128_pp_split(const AttnArgs& a, hipStream_t stream) 
   attn_fwd_pp_kernel<true><<<rows * unsigned(a.split), kThreads, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  return launch_attn_split_merge(a, stream);
+}
+
+hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream) {
+  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
   attn_split_merge_kernel<<<rows, 256, 0, stream>>>(a);
   return hipGetLastError();
 }

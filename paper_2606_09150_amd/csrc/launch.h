@@ -112,9 +112,13 @@ hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_w32(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_pp_split(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream);
+// combines the split-KV partials in a.work into O and LSE
+hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream);
 
 inline hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
-  return a.T == 128 ? launch_attn_fwd_t128_pp(a, stream) : launch_attn_fwd_t64(a, stream);
+  return a.T == 128 ? launch_attn_fwd_t128_tri(a, stream) : launch_attn_fwd_t64(a, stream);
 }
 
 }  // namespace uf

@@ -465,7 +465,7 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
     return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, split_work_bytes(kv, n_split));
   a.split = n_split;
   a.work = static_cast<float*>(d_work);
-  hipError_t e = uf::launch_attn_fwd_t128_pp_split(a, static_cast<hipStream_t>(stream));
+  hipError_t e = uf::launch_attn_fwd_t128_tri_split(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));
   return ok();
 }
