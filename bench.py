@@ -37,9 +37,10 @@ D = 128
 # Measured HBM traffic of the attention kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
 # scaled by a plain copy of known size), valid only for the kernel sources it was
 # measured on: their SHA-256 is recorded beside the figure.
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_fwd_pp_1k_traffic.md")
-ATTN_SOURCES = ("paper_2606_09150_amd/csrc/kernels/attn_fwd_pp.hip",
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attn_fwd_tri_1k_traffic.md")
+ATTN_SOURCES = ("paper_2606_09150_amd/csrc/kernels/attn_fwd_tri.hip",
                 "paper_2606_09150_amd/csrc/kernels/attn_common.h",
+                "paper_2606_09150_amd/csrc/kernels/kv_append.hip",
                 "paper_2606_09150_amd/csrc/launch.h")
 
 

@@ -96,17 +96,20 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(BwdArgs a) {
 __device__ inline int swz_perm(int c) { return (c & ~10) | ((c & 2) << 2) | ((c & 8) >> 2); }
 __device__ inline int swz_f(int r) { return (r & 8) | ((r & 3) << 1) | (((r >> 2) ^ (r >> 3)) & 1); }
 
-// Copy one 32 KB tile global -> LDS in that layout: copy i of wave w fills
-// LDS chunks [64*(4i + w), +64), i.e. row 16i + 4w + lane/16, position
-// lane%16.  The row's low four bits do not depend on i, so one per-lane
-// source offset serves all eight copies, with 4 KB steps on the scalar base.
-__device__ inline uint32_t copy_offset(int wave, int lane) {
+// Copy one 32 KB K or V^T tile of a page global -> LDS in that layout: copy i
+// of wave w fills LDS chunks [64*(4i + w), +64), i.e. row 16i + 4w + lane/16,
+// position lane%16.  The row's low four bits do not depend on i, so one
+// per-lane source offset serves all eight copies, with 2 KB steps on the
+// scalar base: a page keeps the 16-byte chunks 0..7 and 8..15 of every row in
+// two blocks of 128-byte rows, 16 KB apart.
+__device__ inline uint32_t page_chunk(int r, int c) { return uint32_t((c >> 3) * 16384 + r * 128 + (c & 7) * 16); }
+__device__ inline uint32_t copy_offset_page(int wave, int lane) {
   const int r = 4 * wave + (lane >> 4);
-  return uint32_t(r * 256 + swz_perm((lane & 15) ^ swz_f(r)) * 16);
+  return page_chunk(r, swz_perm((lane & 15) ^ swz_f(r)));
 }
-__device__ inline void copy_tile(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
+__device__ inline void copy_tile_page(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) dma16(src + i * 4096, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 4096u);
+  for (int i = 0; i < 8; ++i) dma16(src + i * 2048, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 4096u);
 }
 
 // LDS byte offset of bf16 element (r, c) of a tile.
@@ -219,6 +222,14 @@ __device__ inline void copy_tile8(const uint8_t* src, uint32_t lds_tile, uint32_
 #pragma unroll
   for (int i = 0; i < 4; ++i) dma16(src + i * 8192, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 8192u);
 }
+__device__ inline uint32_t copy_offset8_page(int wave, int lane) {
+  const int r = 4 * wave + (lane >> 4);
+  return page_chunk(r, swz_perm((lane & 15) ^ swz_f(r & 15)));
+}
+__device__ inline void copy_tile8_page(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16(src + i * 4096, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 8192u);
+}
 
 __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   __shared__ uint4 sQ[2][kT * 16], sO[2][kT * 16];   // Q and dO rows, two query tiles (128 KB)
@@ -251,9 +262,9 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   if (grp == 0) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks)
-      bop[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + size_t(key) * 256 + (2 * ks + hl) * 16));
+      bop[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + page_chunk(key, 2 * ks + hl)));
   }
-  copy_tile8(page + kTile, lds_addr(&sO[1][0]), voff, wave);
+  copy_tile8_page(page + kTile, lds_addr(&sO[1][0]), copy_offset8_page(wave, lane), wave);
 
   // kept query tiles, ascending
   if (wave == 0) {
@@ -435,7 +446,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
-  const uint32_t voff = copy_offset(wave, lane);
+  const uint32_t voff = copy_offset_page(wave, lane);
   const int q = wave * 32 + ln;                 // this lane's query (result column)
   const lds_u8* lk = (const lds_u8*)sK;
   const lds_u8* lv = (const lds_u8*)sV;
@@ -480,8 +491,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
       page = head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
     }
     __syncthreads();                            // previous tile consumed
-    copy_tile(page, lds_addr(sK), voff, wave);
-    copy_tile(page + kTile, lds_addr(sV), voff, wave);
+    copy_tile_page(page, lds_addr(sK), voff, wave);
+    copy_tile_page(page + kTile, lds_addr(sV), voff, wave);
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
 #pragma unroll

@@ -1,4 +1,5 @@
-// attn_fwd: block-sparse chunk-causal attention forward on gfx950.
+// attn_fwd (64-token tiles): block-sparse chunk-causal attention forward on
+// gfx950.
 //
 // For one (b, h, query tile i) the workgroup walks the kept key tiles of its
 // list in ascending logical order (Eq. 4: attention restricted to the kept
@@ -268,12 +269,6 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
   attn_fwd_kernel<64><<<blocks, 128, 0, stream>>>(a);
-  return hipGetLastError();
-}
-
-hipError_t launch_attn_fwd_t128_w32(const AttnArgs& a, hipStream_t stream) {
-  const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
-  attn_fwd_kernel<128><<<blocks, 256, 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -20,11 +20,11 @@
 // unit spans two phases, and two waves issuing VALU work side by side reach
 // about twice the issue rate of one.
 //
-// Products.  As in the two-group kernel: K and V^T from LDS as the A operand,
-// Q^T and P^T as B operands in registers, every lane owns one query column
-// (row max and sum need one permlane32 exchange), and the weights rounded to
-// bf16 in place are the PV operand (V pages keep the keys of each group of 16
-// in swap23 order, the k-slot order of the S^T result lanes).
+// Products.  K and V^T come from LDS as the A operand, Q^T and P^T are B
+// operands in registers, every lane owns one query column (row max and sum
+// need one permlane32 exchange), and the weights rounded to bf16 in place are
+// the PV operand (V pages keep the keys of each group of 16 in swap23 order,
+// the k-slot order of the S^T result lanes).
 //
 // Memory.  Half tiles (16 KB: 64 keys of K, or 64 keys of V^T with rows d and
 // d+64 side by side) are copied HBM -> LDS by global_load_lds, 16 bytes per
@@ -33,7 +33,9 @@
 // is a 3-bit XOR pattern chosen so that operand reads (16 bytes per lane, 32
 // rows) are free of bank conflicts whether 8 or 16 lanes share a cycle; the
 // lane's source offset then depends on c only through c%2, and the operand
-// read offsets of a lane take four values plus compile-time constants.
+// read offsets of a lane take four values plus compile-time constants.  The
+// pages keep K and V^T in blocks of 64 columns (128-byte rows), so each copy
+// reads one contiguous kilobyte: eight consecutive rows of one block.
 // Buffers: one K slot per group (K of unit u+3 is copied by group u%3 in its
 // first softmax phase, right after the MFMA phase that read K of unit u) and
 // six V slots (V of unit u+3 copied in the group's second softmax phase,
@@ -126,12 +128,12 @@ __device__ __forceinline__ void tri_mfma(TriState& st, const bf16x8 (&qf)[8], co
 }
 
 // The four 1-KB copies of a wave for one half tile: copy t is copy c = q + 4t
-// of the half tile (q = the wave's query block), source src + 8192 (t % 2) +
+// of the half tile (q = the wave's query block), source src + 4096 (t % 2) +
 // step (t / 2) plus the lane offset, LDS destination lds + 4096 t.
 struct HalfCopy {
   const uint8_t* src;
   uint32_t lds;
-  uint32_t step;    // source bytes per c/8: 128 for K, 16384 for V^T
+  uint32_t step;    // source bytes per c/8: the next K block (16384) or the next 64 rows of V^T (8192)
   bool on;
 };
 // A pointer that is the same on every lane, held in scalar registers.
@@ -143,7 +145,7 @@ __device__ __forceinline__ const uint8_t* uniform_ptr(const uint8_t* q) {
   return reinterpret_cast<const uint8_t*>(lo | (hi << 32));
 }
 __device__ __forceinline__ void half_copy(const HalfCopy& cp, uint32_t lane_off, int t) {
-  dma16(uniform_ptr(cp.src + 8192 * (t & 1) + cp.step * (t >> 1)), lane_off, cp.lds + 4096u * uint32_t(t));
+  dma16(uniform_ptr(cp.src + 4096 * (t & 1) + cp.step * (t >> 1)), lane_off, cp.lds + 4096u * uint32_t(t));
 }
 
 // Weights of key block H (the lane's 16 scores of keys 32H..32H+31) at the
@@ -304,7 +306,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   uint32_t rd[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) rd[j] = uint32_t(128 * ln + 16 * ((2 * j + hl) ^ swz(ln & 15)));
-  const uint32_t lane_off = uint32_t((lane >> 3) * 256 + (((lane & 7) ^ swz(8 * (qw & 1) + (lane >> 3))) * 16));
+  const uint32_t lane_off = uint32_t((lane >> 3) * 128 + (((lane & 7) ^ swz(8 * (qw & 1) + (lane >> 3))) * 16));
   const uint8_t* lds = reinterpret_cast<const uint8_t*>(&sbuf[0][0]);
   const uint32_t lds_base = lds_addr(&sbuf[0][0]) + 1024u * uint32_t(qw);
 
@@ -340,11 +342,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
     r.valid = min(max(tile_valid(a.tv, t, a.NT, a.tail, kT) - 64 * (w & 1), 0), 64);
     return r;
   };
+  // page bytes: K block j (dimensions 64j..) at 16384 j, rows of 128 bytes;
+  // V^T block j (keys 64j..) at 32768 + 16384 j.  Copy c of a half: K rows
+  // 64(w%2) + 8(c%8) .. of block c/8; V^T rows 8(c%8) + 64(c/8) .. of block w%2.
   auto kcopy = [&](const Unit& un, int w, int kbuf) {
-    return HalfCopy{un.page + 16384 * (w & 1) + 2048 * qw, lds_base + uint32_t(kbuf) * kHalf, 128u, w < U};
+    return HalfCopy{un.page + 8192 * (w & 1) + 1024 * qw, lds_base + uint32_t(kbuf) * kHalf, 16384u, w < U};
   };
   auto vcopy = [&](const Unit& un, int w, int vbuf) {
-    return HalfCopy{un.page + 32768 + 128 * (w & 1) + 2048 * qw, lds_base + uint32_t(vbuf) * kHalf, 16384u, w < U};
+    return HalfCopy{un.page + 32768 + 16384 * (w & 1) + 1024 * qw, lds_base + uint32_t(vbuf) * kHalf, 8192u, w < U};
   };
   auto issue = [&](const HalfCopy& cp) {
     if (cp.on)
@@ -517,6 +522,59 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   }
 }
 
+// Split-KV merge: one workgroup per row; lane (query, half) combines the
+// row's partials for 64 dims: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+__global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
+  const int row = blockIdx.x;
+  const int qt = row % a.NT;
+  const int bh = row / a.NT;
+  const int h = bh % a.H;
+  const int b = bh / a.H;
+  const int ql = threadIdx.x >> 1;
+  const int half = threadIdx.x & 1;
+  const int qrow = qt * kT + ql;
+  if (qrow >= a.L) return;
+  const float2* ml = reinterpret_cast<const float2*>(a.work + size_t(a.B) * a.H * a.NT * a.split * kT * kD);
+  float mm = -INFINITY;
+  for (int s = 0; s < a.split; ++s) {
+    const float2 v = ml[(size_t(row) * a.split + s) * kT + ql];
+    if (v.y > 0.f) mm = fmaxf(mm, v.x);
+  }
+  float acc[64];
+#pragma unroll
+  for (int d = 0; d < 64; ++d) acc[d] = 0.f;
+  float l = 0.f;
+  for (int s = 0; s < a.split; ++s) {
+    const size_t wrow = size_t(row) * a.split + s;
+    const float2 v = ml[wrow * kT + ql];
+    if (!(v.y > 0.f)) continue;   // empty slice
+    const float w = __builtin_amdgcn_exp2f(v.x - mm);
+    l += v.y * w;
+    const float4* op = reinterpret_cast<const float4*>(a.work + (wrow * kT + ql) * kD + 64 * half);
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const float4 o = op[c];
+      acc[4 * c + 0] += o.x * w;
+      acc[4 * c + 1] += o.y * w;
+      acc[4 * c + 2] += o.z * w;
+      acc[4 * c + 3] += o.w * w;
+    }
+  }
+  const float inv = (l > 0.f) ? 1.f / l : 0.f;
+  uint16_t* out = a.o + ((size_t(b) * a.L + qrow) * a.H + h) * kD + 64 * half;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    uint4 w;
+    w.x = pack_bf16x2(acc[8 * c + 0] * inv, acc[8 * c + 1] * inv);
+    w.y = pack_bf16x2(acc[8 * c + 2] * inv, acc[8 * c + 3] * inv);
+    w.z = pack_bf16x2(acc[8 * c + 4] * inv, acc[8 * c + 5] * inv);
+    w.w = pack_bf16x2(acc[8 * c + 6] * inv, acc[8 * c + 7] * inv);
+    reinterpret_cast<uint4*>(out)[c] = w;
+  }
+  if (a.lse != nullptr && half == 0)
+    a.lse[(size_t(b) * a.H + h) * a.L + qrow] = (l > 0.f) ? (mm + log2f(l)) * 0.69314718055994531f : -INFINITY;
+}
+
 }  // namespace
 
 hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream) {
@@ -531,6 +589,12 @@ hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream)
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_attn_split_merge(a, stream);
+}
+
+hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream) {
+  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
+  attn_split_merge_kernel<<<rows, 256, 0, stream>>>(a);
+  return hipGetLastError();
 }
 
 }  // namespace uf

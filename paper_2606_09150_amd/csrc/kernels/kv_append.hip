@@ -3,10 +3,13 @@
 // Appending the new chunk's keys and values to the layer's KV cache is the
 // cache side of chunk-wise streaming generation (Sec. 2.3.2, dynamic cache
 // management; Alg. 3, inference part).  One workgroup fills one page
-// (slot, b, h, tile t): K is copied row for row ([T][D], 16-byte loads and
-// stores); V is staged in LDS and written transposed ([D][T]) with the keys of
-// every group of 16 stored in swap23 order, which is the order in which the
-// attention kernel's 32x32x16 MFMA consumes them.  Rows past the chunk end get
+// (slot, b, h, tile t): K is copied row for row (16-byte loads and stores); V
+// is staged in LDS and written transposed with the keys of every group of 16
+// stored in swap23 order, which is the order in which the attention kernel's
+// 32x32x16 MFMA consumes them.  128-token pages store both as blocks of 64
+// columns (K: [2][T][64], dimension halves; V^T: [2][D][64], key halves), so
+// that 64 keys of either are 8 KB pieces of 128-byte rows; 64-token pages keep
+// K as [T][D] and V^T as [D][T].  Rows past the chunk end get
 // the pad value.  The page's pooled key (the block-mean pooling of Eq. 4,
 // Sec. 2.3.1 (b)) is written beside it: the float32 mean of the valid K rows,
 // summed in token order and divided once by their count, so that the top-k
@@ -24,6 +27,7 @@ template <int T>
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a) {
   constexpr int kRowChunks = kD / 8;          // 16-byte chunks per K/V input row
   constexpr int kStage = kRowChunks + 1;      // LDS row stride in chunks (272 bytes)
+  constexpr bool kBlocks = T == 128;          // 64-column blocks (see above)
   __shared__ uint4 vstage[T * kStage];
 
   const int page = blockIdx.x;                // (b*H + h)*NT + t
@@ -47,7 +51,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a) {
       kk = *reinterpret_cast<const uint4*>(a.k + off);
       vv = *reinterpret_cast<const uint4*>(a.v + off);
     }
-    kdst[c] = kk;
+    kdst[kBlocks ? (cc >> 3) * (T * 8) + r * 8 + (cc & 7) : c] = kk;
     vstage[r * kStage + cc] = vv;
   }
   __syncthreads();
@@ -65,7 +69,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendArgs a) {
       const uint32_t hi = vs[swap23(p0 + 2 * e + 1) * (kStage * 8) + d];
       w[e] = lo | (hi << 16);
     }
-    vdst[c] = make_uint4(w[0], w[1], w[2], w[3]);
+    vdst[kBlocks ? (p0 >> 6) * (kD * 8) + d * 8 + ((p0 & 63) >> 3) : c] = make_uint4(w[0], w[1], w[2], w[3]);
   }
 
   // Pooled key: the valid K rows are staged again (L2-resident since the

@@ -10,7 +10,9 @@
 
 namespace uf {
 
-// Bytes of one page: K [T][D] bf16 followed by V^T [D][T] bf16.
+// Bytes of one page: K, then V^T, T*D bf16 each.  128-token pages keep both
+// in blocks of 64 columns (K: [2][T][64] dimension halves, V^T: [2][D][64]
+// key halves); 64-token pages hold K [T][D] and V^T [D][T].
 __host__ __device__ inline size_t page_bytes(int T, int D) { return size_t(4) * size_t(T) * size_t(D); }
 
 // Column of key r inside its group of 16 in a V^T page row: bits 2 and 3
@@ -109,9 +111,6 @@ struct PermuteArgs {
 };
 hipError_t launch_block_permute(const PermuteArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
-hipError_t launch_attn_fwd_t128_w32(const AttnArgs& a, hipStream_t stream);
-hipError_t launch_attn_fwd_t128_pp(const AttnArgs& a, hipStream_t stream);
-hipError_t launch_attn_fwd_t128_pp_split(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream);
 // combines the split-KV partials in a.work into O and LSE

@@ -1,5 +1,6 @@
 """uf_kv_append: pages read back bit for bit against the layout documented in
-include/uf.h (K rows, V transposed with swap23 key order, padded tails)."""
+include/uf.h (K and V transposed, in 64-column blocks for 128-token pages;
+swap23 key order; padded tails)."""
 
 import numpy as np
 import pytest
@@ -9,6 +10,21 @@ import synth
 from tests.gpu_common import log, require_gpu
 
 pytestmark = pytest.mark.gpu
+
+
+def _page_views(raw, T, D):
+    """Logical K [T][D] and V^T [D][T] of a page (uf.h: 128-token pages keep
+    both as two blocks of 64 columns, 64-token pages as plain rows)."""
+    half = raw.size // 2
+    k = raw[:half].view(np.uint16)
+    v = raw[half:].view(np.uint16)
+    if T == 128:
+        k = k.reshape(2, T, 64).transpose(1, 0, 2).reshape(T, D)
+        v = v.reshape(2, D, 64).transpose(1, 0, 2).reshape(D, T)
+    else:
+        k = k.reshape(T, D)
+        v = v.reshape(D, T)
+    return k, v
 
 
 def _swap23(p):
@@ -49,8 +65,7 @@ def test_pages_read_back(B, L, H, T, poison):
             for h in range(H):
                 for t in range(nt):
                     off = (((slot * B + b) * H + h) * nt + t) * page
-                    kpage = pool[off:off + 2 * T * D].view(np.uint16).reshape(T, D)
-                    vpage = pool[off + 2 * T * D:off + page].view(np.uint16).reshape(D, T)
+                    kpage, vpage = _page_views(pool[off:off + page], T, D)
                     valid = tail if t == nt - 1 else T
                     assert np.array_equal(kpage[:valid], kb[b, t * T:t * T + valid, h, :])
                     assert (kpage[valid:] == pad).all()
