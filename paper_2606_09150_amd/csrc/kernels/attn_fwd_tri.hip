@@ -62,7 +62,8 @@ using namespace attn;
 constexpr int kT = 128;
 constexpr int kThreads = 768;          // twelve waves
 constexpr uint32_t kHalf = 16384;      // bytes of a half-tile buffer
-constexpr int kVBase = 3;              // buffers 0..2: K slot of each group, 3..8: V slots
+// LDS buffers of group g: 3g (V slot g), 3g+1 (V slot g+3), 3g+2 (its K slot)
+constexpr int kGroupBytes = 3 * kHalf;
 constexpr int kBuffers = 9;
 constexpr float kSumBound = 4096.0f;   // lane row-sum bound of one unit's 32 weights
 
@@ -93,27 +94,27 @@ __device__ __forceinline__ void sync_vm() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// MFMA phase: O^T += V^T P^T of the previous unit (V^T in buffer VB of the
-// group's V buffers, read at rv + VB * kHalf) and S^T = K Q^T of the current
-// unit (K in buffer KB, read at rd).  Every LDS offset beyond the lane's base
-// fits the 16-bit immediate.
-template <int KB, int VB>
-__device__ __forceinline__ void tri_mfma(TriState& st, const bf16x8 (&qf)[8], const uint32_t (&rd)[4],
-                                         const uint32_t (&rv)[4], const uint8_t* lds) {
+// MFMA phase: O^T += V^T P^T of the previous unit (V^T in the group's buffer
+// VB, 0 or 1) and S^T = K Q^T of the current unit (K in the group's buffer 2).
+// rg holds the lane's read offsets within the group's 48 KB, so that every
+// further offset fits the 16-bit immediate of the LDS instructions.
+template <int VB>
+__device__ __forceinline__ void tri_mfma(TriState& st, const bf16x8 (&qf)[8], const uint32_t (&rg)[4],
+                                         const uint8_t* lds) {
   const uint8_t* vb = lds + VB * kHalf;
-  const uint8_t* kb = lds + KB * kHalf;
+  const uint8_t* kb = lds + 2 * kHalf;
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) {
-      const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint4*>(vb + rv[j] + 4096 * mb));
+      const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint4*>(vb + rg[j] + 4096 * mb));
       st.o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, st.p[j], st.o[mb], 0, 0, 0);
     }
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(kb + rd[ks & 3] + 4096 * h + 8192 * (ks >> 2)));
+      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const uint4*>(kb + rg[ks & 3] + 4096 * h + 8192 * (ks >> 2)));
       st.s[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], ks == 0 ? f32x16{} : st.s[h], 0, 0, 0);
     }
   // operand reads: kAhead in flight, then one per MFMA
@@ -155,16 +156,19 @@ template <int H, bool COPIES>
 __device__ __forceinline__ float tri_weights(TriState& st, float c2, const HalfCopy& cp, uint32_t lane_off) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float rs = 0.f;
-  if (COPIES && cp.on) {
-    half_copy(cp, lane_off, 0);
-    half_copy(cp, lane_off, 1);
-  }
 #pragma unroll
   for (int jj = 0; jj < 2; ++jj) {
-    if (COPIES && cp.on) half_copy(cp, lane_off, 2 + jj);
     bf16x2 pr[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
+      // a copy before every second pair of weights, fenced by scheduling
+      // barriers (the guarded copies still end up at the start of the phase,
+      // but the fences keep the weights in this order, which measured faster)
+      if (COPIES && (e & 1) == 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (cp.on) half_copy(cp, lane_off, 2 * jj + (e >> 1));
+        __builtin_amdgcn_sched_barrier(0);
+      }
       const float x0 = __builtin_fmaf(st.s[H][8 * jj + 2 * e], c2, -st.moff);
       const float x1 = __builtin_fmaf(st.s[H][8 * jj + 2 * e + 1], c2, -st.moff);
       pr[e] = bf16x2{(__bf16)__builtin_amdgcn_exp2f(x0), (__bf16)__builtin_amdgcn_exp2f(x1)};
@@ -369,46 +373,47 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
 
   if (U > 0) {
     // The first PV of each group (unit -3, -2 or -1) multiplies zero weights
-    // by V^T buffers 6..8, which no copy has filled yet: zero them.
-    {
-      uint4* z = &sbuf[kVBase + 3][0];
+    // by V^T buffers 1, 4 and 7 (V slots 3..5), which no copy has filled yet:
+    // zero them.
 #pragma unroll
-      for (int i = 0; i < 4; ++i) z[tid + kThreads * i] = make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+      const int k = tid + kThreads * i;   // 0 .. 3071: 1024 uint4 per buffer
+      sbuf[3 * (k >> 10) + 1][k & 1023] = make_uint4(0, 0, 0, 0);
     }
     // Each group runs its own copy of the phase sequence (template G); all
     // pass the same P barriers.  Unit u of group G: MFMA phase u, softmax
-    // phases u+1 and u+2.  K of unit u lives in buffer G, V of unit u in V
-    // slot u % 6 (buffer 3 + u % 6).
+    // phases u+1 and u+2.  K of unit u lives in buffer 3G+2, V of unit u in
+    // V slot u % 6 (buffer 3G, or 3G+1 when u % 6 >= 3).
     auto run = [&](auto Gc) {
       constexpr int G = decltype(Gc)::value;
-      // the group's V buffers are kVBase + G and kVBase + G + 3: lane bases
-      // for them, kept opaque so that the compiler does not fold the buffer
-      // offset back into immediates too large for the LDS instructions
-      uint32_t rv[4];
+      // lane read offsets within the group's buffers, kept opaque so that
+      // the compiler does not fold the group offset back into immediates too
+      // large for the LDS instructions
+      uint32_t rg[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        rv[j] = rd[j] + uint32_t(kVBase + G) * kHalf;
-        asm volatile("" : "+v"(rv[j]));
+        rg[j] = rd[j] + uint32_t(G) * kGroupBytes;
+        asm volatile("" : "+v"(rg[j]));
       }
       Unit cur = unit(G);
       // prologue: K of units 0 and 1, V of unit 0; later copies follow the
       // steady-state rule (K[u+3] in phase u+1, V[u+3] in phase u+2)
       if (G == 0) {
-        issue(kcopy(cur, 0, 0));
-        issue(vcopy(cur, 0, kVBase + 0));
+        issue(kcopy(cur, 0, 2));
+        issue(vcopy(cur, 0, 0));
       }
-      if (G == 1) issue(kcopy(cur, 1, 1));
+      if (G == 1) issue(kcopy(cur, 1, 5));
       sync_vm<0>();
       int ph = 0;
       if (G == 1) {   // phase 0, second softmax phase of unit -2: copy V[1]
-        issue(vcopy(cur, 1, kVBase + 1));
+        issue(vcopy(cur, 1, 3));
         if (1 < U) sync_vm<4>(); else sync_vm<0>();
         ph = 1;
       }
       if (G == 2) {   // phases 0 and 1, softmax phases of unit -1: copy K[2], V[2]
-        issue(kcopy(cur, 2, 2));
+        issue(kcopy(cur, 2, 8));
         sync_vm<63>();
-        issue(vcopy(cur, 2, kVBase + 2));
+        issue(vcopy(cur, 2, 6));
         if (2 < U) sync_vm<4>(); else sync_vm<0>();
         ph = 2;
       }
@@ -417,16 +422,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
       // Q = 1: u % 6 == G+3 and the other way round.
       auto cycle = [&](auto Qc, int u) -> bool {
         constexpr int Q = decltype(Qc)::value;
-        constexpr int VPV = 3 * (1 - Q);         // V of unit u-3 (relative to buffer kVBase + G)
-        constexpr int VNEW = kVBase + G + VPV;   // V of unit u+3 (same slot, freed by the PV)
+        constexpr int VPV = 1 - Q;               // V of unit u-3: the group's buffer VPV
+        constexpr int VNEW = 3 * G + VPV;        // V of unit u+3 (same slot, freed by the PV)
         __builtin_amdgcn_s_setprio(1);
-        tri_mfma<G, VPV>(st, qf, rd, rv, lds);
+        tri_mfma<VPV>(st, qf, rg, lds);
         __builtin_amdgcn_s_setprio(0);
         sync_vm<63>();
         if (++ph == P) return false;
         // first softmax phase: K of unit u+3 into buffer G
         const Unit nxt = unit(u + 3);
-        const HalfCopy kc = kcopy(nxt, u + 3, G);
+        const HalfCopy kc = kcopy(nxt, u + 3, 3 * G + 2);
         tri_first(st, cur.valid, hl, c2, kc, lane_off);
         pin_first(st);
         sync_vm<63>();
