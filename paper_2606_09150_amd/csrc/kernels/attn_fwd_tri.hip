@@ -45,11 +45,15 @@
 // barrier after it publishes them to the group.
 //
 // Softmax in base 2 with a lazy offset m per lane: weights exp2(c2 s - m),
-// c2 = scale*log2(e).  The offset is raised only when the bf16-rounded
-// weights of a unit sum to more than kSumBound on some lane (or on a lane's
-// first valid key); then the exact max is taken, O and l are rescaled, and
-// the unit's weights are recomputed.  The check runs once per unit, in the
-// second softmax phase, while the raw scores of both halves are still held.
+// c2 = scale*log2(e).  The offset is raised only when the weights of a half
+// unit sum to more than kSumBound on some lane (or on a lane's first valid
+// key); then the exact max is taken, O and l are rescaled, and the weights
+// are recomputed (first softmax phase: from the max over the whole unit;
+// second: by a whole number of octaves, see tri_second).  The row sum adds
+// the fp32 weights before their rounding to bf16: the normalisation then
+// differs from the sum of the rounded weights by at most 2^-9 relative, and
+// fp32 adds are cheaper here than v_dot2 over the packed weights, which
+// slows down next to a stream of MFMAs.
 #include "attn_common.h"
 
 #include <type_traits>
@@ -65,7 +69,7 @@ constexpr uint32_t kHalf = 16384;      // bytes of a half-tile buffer
 // LDS buffers of group g: 3g (V slot g), 3g+1 (V slot g+3), 3g+2 (its K slot)
 constexpr int kGroupBytes = 3 * kHalf;
 constexpr int kBuffers = 9;
-constexpr float kSumBound = 4096.0f;   // lane row-sum bound of one unit's 32 weights
+constexpr float kSumBound = 4096.0f;   // lane row-sum bound of one half unit's 16 weights
 
 // 3-bit XOR pattern of LDS row r (r % 16): bijective in bits 0..2 for either
 // value of bit 3, and in bits 1..3 for either value of bit 0.
@@ -137,6 +141,18 @@ struct HalfCopy {
   uint32_t step;    // source bytes per c/8: the next K block (16384) or the next 64 rows of V^T (8192)
   bool on;
 };
+// j / NT for 0 <= j < 2^31 from d = (2^64 - 1) / NT: ((j + 1) * d) >> 64 in
+// scalar integer arithmetic (a division by a run-time value would otherwise
+// use vector float instructions in the softmax waves).  With d = (2^64 - r) / NT,
+// 0 < r <= NT, the product is (j + 1) / NT minus less than 2^-32, which floors
+// to j / NT.
+__device__ __forceinline__ int div_nt(uint32_t j, uint64_t d) {
+  const uint64_t x = uint64_t(j) + 1u;
+  const uint64_t lo = x * uint32_t(d);
+  const uint64_t hi = x * uint32_t(d >> 32);
+  return int((hi + (lo >> 32)) >> 32);
+}
+
 // A pointer that is the same on every lane, held in scalar registers.
 __device__ __forceinline__ const uint8_t* uniform_ptr(const uint8_t* q) {
   const uint64_t p = reinterpret_cast<uint64_t>(q);
@@ -151,10 +167,9 @@ __device__ __forceinline__ void half_copy(const HalfCopy& cp, uint32_t lane_off,
 
 // Weights of key block H (the lane's 16 scores of keys 32H..32H+31) at the
 // current offset into P^T steps 2H, 2H+1; returns the lane's sum of the
-// bf16-rounded weights.  The copies of `cp` are issued along the way.
+// weights (before rounding).  The copies of `cp` are issued along the way.
 template <int H, bool COPIES>
 __device__ __forceinline__ float tri_weights(TriState& st, float c2, const HalfCopy& cp, uint32_t lane_off) {
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float rs = 0.f;
 #pragma unroll
   for (int jj = 0; jj < 2; ++jj) {
@@ -171,8 +186,9 @@ __device__ __forceinline__ float tri_weights(TriState& st, float c2, const HalfC
       }
       const float x0 = __builtin_fmaf(st.s[H][8 * jj + 2 * e], c2, -st.moff);
       const float x1 = __builtin_fmaf(st.s[H][8 * jj + 2 * e + 1], c2, -st.moff);
-      pr[e] = bf16x2{(__bf16)__builtin_amdgcn_exp2f(x0), (__bf16)__builtin_amdgcn_exp2f(x1)};
-      rs = __builtin_amdgcn_fdot2_f32_bf16(pr[e], ones, rs, false);
+      const float w0 = __builtin_amdgcn_exp2f(x0), w1 = __builtin_amdgcn_exp2f(x1);
+      pr[e] = bf16x2{(__bf16)w0, (__bf16)w1};
+      rs += w0 + w1;
     }
     st.p[2 * H + jj] = __builtin_shufflevector(__builtin_shufflevector(pr[0], pr[1], 0, 1, 2, 3),
                                                __builtin_shufflevector(pr[2], pr[3], 0, 1, 2, 3),
@@ -340,7 +356,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
       r.page = head_pages + size_t(a.slot_of[0]) * slot_stride;
       return r;
     }
-    const int pos = j / a.NT;
+    const int pos = div_nt(uint32_t(j), a.nt_div);
     const int t = j - pos * a.NT;
     r.page = head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
     r.valid = min(max(tile_valid(a.tv, t, a.NT, a.tail, kT) - 64 * (w & 1), 0), 64);

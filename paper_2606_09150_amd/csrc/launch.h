@@ -95,6 +95,7 @@ struct AttnArgs {
   const int32_t* counts;  // [rows]
   const int32_t* idx;     // [rows][nk_cap]
   int32_t B, H, L, T, NT, tail, nk, nk_cap;
+  uint64_t nt_div;        // (2^64 - 1) / NT: j / NT == ((j + 1) * nt_div) >> 64 for 0 <= j < 2^31
   float scale;            // softmax scale
   float scale_log2;       // scale * log2(e)
   int32_t split;          // list slices per row (split-KV), 1 = whole rows

@@ -413,6 +413,7 @@ int attn_args(const uf_kv* kv, const void* d_q, const void* d_lists, float scale
   a.L = kv->d.chunk_tokens;
   a.T = kv->d.tile;
   a.NT = kv->nt;
+  a.nt_div = UINT64_MAX / uint64_t(kv->nt);
   a.tail = kv->tail;
   a.nk = int32_t(kv->live.size()) * kv->nt;
   a.nk_cap = kv->nk_cap;
