@@ -48,6 +48,10 @@ SMALL = [
     (1, 1000, 2, 128, 5, True, 7, 0.25),
     (1, 256, 1, 128, 1, False, 1, 0.0),
     (1, 640, 4, 128, 3, False, 4, 0.0),
+    # one tile per chunk: every row keeps a single tile (two 64-key units) ...
+    (1, 100, 2, 128, 1, False, 1, 0.0),
+    # ... or the pinned tile and the current one (four units)
+    (2, 100, 2, 128, 2, True, 2, 1.0),
 ]
 
 
