@@ -158,12 +158,12 @@ typedef struct {
  * then as many pooled keys of D float32 each (4*D bytes).
  * Page of (slot s, b, h, tile t) starts at ((((s*B + b)*H + h)*NT + t) * 4*T*D);
  * it holds K (row r = token t*T + r of the chunk), then V transposed (row d =
- * dimension d), both in bf16 and both cut into blocks of 64 columns stored one
- * after the other: K as D/64 = 2 blocks of T rows x 64 dimensions (block j holds
- * dimensions 64j..64j+63), then V^T as T/64 blocks of D rows x 64 keys (block j
- * holds keys 64j..64j+63) -- for T = 64 that is V^T as D rows of T keys.  T = 64
- * pages keep K as T rows of D.  In V^T the keys of each group of 16 are stored
- * with bits 2 and 3 of the key index swapped (column p of a block holds key
+ * dimension d), both bf16, T*D elements each.  T = 128: both are stored as two
+ * blocks of 64 columns, one after the other: K as [2][T][64] (block j holds
+ * dimensions 64j..64j+63 of every key), V^T as [2][D][64] (block j holds keys
+ * 64j..64j+63 of every dimension).  T = 64: K as [T][D] and V^T as [D][T].
+ * In V^T the keys of each group of 16 are stored with bits 2 and 3 of the key
+ * index swapped (column p of a block holds key
  * (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1) of that block).  Rows past the
  * chunk end are 0 (9984.0 under UF_F_POISON_PAD).  The pooled key of the same page, the float32
  * mean of its valid K rows (the key pooling of Eq. 4, written by append), starts
