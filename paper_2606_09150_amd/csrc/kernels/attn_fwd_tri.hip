@@ -440,9 +440,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
         constexpr int Q = decltype(Qc)::value;
         constexpr int VPV = 1 - Q;               // V of unit u-3: the group's buffer VPV
         constexpr int VNEW = 3 * G + VPV;        // V of unit u+3 (same slot, freed by the PV)
-        __builtin_amdgcn_s_setprio(1);
+        // wave priorities: the MFMA phase first, then the first softmax
+        // phase (it issues the K copy), then the second
+        __builtin_amdgcn_s_setprio(2);
         tri_mfma<VPV>(st, qf, rg, lds);
-        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_s_setprio(1);
         sync_vm<63>();
         if (++ph == P) return false;
         // first softmax phase: K of unit u+3 into buffer G
@@ -450,6 +452,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
         const HalfCopy kc = kcopy(nxt, u + 3, 3 * G + 2);
         tri_first(st, cur.valid, hl, c2, kc, lane_off);
         pin_first(st);
+        __builtin_amdgcn_s_setprio(0);
         sync_vm<63>();
         if (++ph == P) return false;
         // second softmax phase: V of unit u+3
