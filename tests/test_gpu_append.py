@@ -74,3 +74,41 @@ def test_pages_read_back(B, L, H, T, poison):
                     ok = keys < valid
                     want_v[:, ok] = vb[b, t * T + keys[ok], h, :].T
                     assert np.array_equal(vpage, want_v)
+
+
+def test_pages_read_back_1k_sampled():
+    """The 1K workload's shape (12 heads, 24,480-token chunks, 128-token
+    pages, five-slot ring): sampled pages of two appended chunks, bit for bit,
+    including the partial last tile."""
+    P = require_gpu()
+    wl = synth.WORKLOADS["1k"]
+    L, H, T, D = wl.chunk_tokens, wl.heads, wl.tile, 128
+    log(f"append 1k sampled pages L={L} H={H} T={T}")
+    win = P.KVWindow(1, H, L, T, wl.max_chunks, wl.pin_sink)
+    chunks = {}
+    for c in range(2):
+        k = synth.custom_tensor((1, L, H, D), 7, c, "k", device="cuda")
+        v = synth.custom_tensor((1, L, H, D), 7, c, "v", device="cuda")
+        win.append(k, v)
+        chunks[c] = (_bits(k), _bits(v))
+    torch.cuda.synchronize()
+    info = win.info()
+    nt, tail = info.nq_tiles, info.tail_valid
+    assert nt == -(-L // T) and tail == L - (nt - 1) * T
+    page = 4 * T * D
+    keys = np.array([_swap23(p) for p in range(T)])
+    for pos in range(info.n_live):
+        slot, seq = win.logical(pos)
+        kb, vb = chunks[seq]
+        for h in (0, 5, H - 1):
+            for t in (0, 1, nt // 2, nt - 2, nt - 1):
+                off = ((slot * H + h) * nt + t) * page
+                raw = win.pool[off:off + page].cpu().numpy()
+                kpage, vpage = _page_views(raw, T, D)
+                valid = tail if t == nt - 1 else T
+                assert np.array_equal(kpage[:valid], kb[0, t * T:t * T + valid, h, :])
+                assert (kpage[valid:] == 0).all()
+                want_v = np.zeros((D, T), dtype=np.uint16)
+                ok = keys < valid
+                want_v[:, ok] = vb[0, t * T + keys[ok], h, :].T
+                assert np.array_equal(vpage, want_v)
