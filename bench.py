@@ -455,7 +455,7 @@ def cpu_baseline(wl, state, target_s):
         "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": f"{wl.name}: head 0, query tiles 1..{n} of {nt} ({n * T} queries x {L * info.n_live} keys, "
-                  f"float64 numpy masked-dense), {sec:.1f} s; throughput in kept-tile FLOP/s",
+                  f"float64 numpy over each row's kept keys), {sec:.1f} s; throughput in kept-tile FLOP/s",
         "seconds": sec,
     }
 

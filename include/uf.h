@@ -1,10 +1,10 @@
 /*
  * uf.h -- C ABI of the MI355X (gfx950) block-sparse chunk-causal attention path.
  *
- * The operation (Ultra Flash, arXiv 2606.09150, Sec. 2.3.1 "Dynamic Block-Sparse
- * Causal Attention", Eq. 4, and Sec. 2.3.2 "Dynamic Cache Management" (iii)):
+ * The operation (Ultra Flash, arXiv 2606.09150, Sec. 2.3.1 (block-sparse causal
+ * attention), Eq. 4, and Sec. 2.3.2 (dynamic cache management) (iii)):
  * a video is generated chunk by chunk; every attention layer keeps a KV cache
- * of earlier chunks (a compact window, App. C "KV cache: 3 temporal windows").
+ * of earlier chunks (a compact window of a few chunks, App. C).
  * The current chunk's queries attend, with scaled softmax attention, over the
  * window's earlier chunks plus the current chunk (the temporal causal mask is
  * chunk-granular: no token-level triangle inside a chunk), restricted per

@@ -8,9 +8,10 @@ It is a plain, slow, obviously correct restatement of what the method computes
 (Ultra Flash, arXiv 2606.09150):
 
 * ``ring``      -- the KV cache window of earlier chunks plus the current chunk
-                   (Sec. 2.3.2, dynamic cache management (iii), "SR cache length
-                   adaptation"; App. C, "KV cache: 3 temporal windows"), with a
-                   pinned first ("sink") chunk and oldest-first eviction.
+                   (Sec. 2.3.2, dynamic cache management (iii): the cache
+                   length of the SR model adapted to a compact window; App. C
+                   gives its size in chunks), with a pinned first ("sink")
+                   chunk and oldest-first eviction.
 * ``keep``      -- the per-(head, query tile) key-tile keep set: the temporal
                    causal mask of Sec. 2.3.1(a) intersected with a seeded
                    Bernoulli content stand-in for the top-k rule of Eq. 4.
@@ -25,6 +26,9 @@ It is a plain, slow, obviously correct restatement of what the method computes
 * ``blocks``    -- the 3-D (b_t, b_h, b_w) block tiling of a chunk's token
                    grid, the block order of tokens, the r x r local window
                    mask M_local, and attention evaluated in raster order.
+* ``mask``      -- the composed block mask of Eq. 4: the content rule (top-k
+                   or the Bernoulli stand-in, forced chunks included), then
+                   M_local, over raster tiles or 3-D blocks.
 * ``backward``  -- gradients dq, dk, dv of the masked attention (the training
                    side of the same forward), float64.
 * ``attention`` -- softmax attention of the current chunk's queries over the
@@ -63,6 +67,7 @@ from .blocks import (
     attention_in_raster,
     attention_in_raster_bwd,
 )
+from .mask import block_sparse_mask
 from .backward import sparse_causal_attention_bwd, sparse_causal_attention_bwd_rows
 from .attention import (
     sparse_causal_attention,
@@ -87,6 +92,7 @@ __all__ = [
     "local_mask",
     "attention_in_raster",
     "attention_in_raster_bwd",
+    "block_sparse_mask",
     "TopkRule",
     "topk_budget",
     "pooled_means",

@@ -20,8 +20,10 @@ of the kept key tiles:
 An empty kept set gives o_r = 0 and lse = -inf (a degenerate case the keep
 rule never produces, since the current chunk is always kept).
 
-Computed as masked dense attention in float64: the excluded scores are set to
--inf before the row maximum.  Inputs are the bf16 values widened exactly.
+Computed in float64 over the window's keys with a keep mask per row: the
+scores of excluded keys take no part in the row maximum and are never
+exponentiated, so their weights are exactly zero.  Inputs are the bf16 values
+widened exactly.
 """
 
 import numpy as np
@@ -48,18 +50,23 @@ def _kept_columns(kept_tiles, L: int, T: int, nt: int, sk: int) -> np.ndarray:
 
 
 def _attend_rows(Q, K, V, cols, scale):
-    """Masked softmax attention of query rows Q [n, D] over keys where cols is True."""
-    n, D = Q.shape
-    if not cols.any():
-        return np.zeros((n, V.shape[1])), np.full(n, -np.inf), np.zeros(n)
+    """Softmax attention of query rows Q [n, D] over the keys where cols is True.
+
+    cols is [Sk] (one keep set for every row) or [n, Sk] (one per row).  A row
+    with no kept key gives o = 0, lse = -inf and a row sum of 0.
+    """
+    n = Q.shape[0]
+    M = np.broadcast_to(np.asarray(cols, dtype=bool), (n, K.shape[0]))
     S = (Q @ K.T) * scale
-    S[:, ~cols] = -np.inf
-    m = S.max(axis=1)
-    P = np.exp(S - m[:, None])
+    m = np.max(S, axis=1, where=M, initial=-np.inf)
+    P = np.zeros_like(S)
+    np.exp(S - m[:, None], out=P, where=M)
     l = P.sum(axis=1)
-    O = (P @ V) / l[:, None]
-    lse = m + np.log(l)
-    rowsum = (P / l[:, None]).sum(axis=1)
+    has = l > 0
+    ls = np.where(has, l, 1.0)
+    O = (P @ V) / ls[:, None]
+    lse = np.where(has, m + np.log(ls), -np.inf)
+    rowsum = (P / ls[:, None]).sum(axis=1)
     return O, lse, rowsum
 
 
@@ -100,6 +107,7 @@ def sparse_causal_attention_rows(ring, q, bits, T: int, scale: float, samples):
     """Same definition, evaluated only at sampled (b, h, row) triples.
 
     samples: iterable of (b, h, r).  Returns O [n, D] and LSE [n] float64.
+    The rows of one head are evaluated together, each over its own keep set.
     """
     q = np.asarray(q, np.float64)
     B, L, H, D = q.shape
@@ -108,14 +116,18 @@ def sparse_causal_attention_rows(ring, q, bits, T: int, scale: float, samples):
     samples = list(samples)
     O = np.zeros((len(samples), D))
     LSE = np.zeros(len(samples))
-    cache = {}
+    by_head = {}
     for n, (b, h, r) in enumerate(samples):
-        if (b, h) not in cache:
-            cache = {(b, h): dense_keys(ring, b, h)}
-        K, V = cache[(b, h)]
-        i = r // T
-        cols = _kept_columns(np.nonzero(bits[b, h, i])[0], L, T, nt, sk)
-        o, lse, _ = _attend_rows(q[b, r : r + 1, h, :], K, V, cols, scale)
-        O[n] = o[0]
-        LSE[n] = lse[0]
+        by_head.setdefault((b, h), []).append(n)
+    for (b, h), ns in by_head.items():
+        K, V = dense_keys(ring, b, h)
+        rows = [samples[n][2] for n in ns]
+        cols = {}
+        for r in rows:
+            if r // T not in cols:
+                cols[r // T] = _kept_columns(np.nonzero(bits[b, h, r // T])[0], L, T, nt, sk)
+        M = np.stack([cols[r // T] for r in rows])
+        o, lse, _ = _attend_rows(q[b, rows, h, :], K, V, M, scale)
+        O[ns] = o
+        LSE[ns] = lse
     return O, LSE

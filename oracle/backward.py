@@ -73,7 +73,8 @@ def sparse_causal_attention_bwd(ring, q, do, bits, T: int, scale: float, heads=N
 
 def sparse_causal_attention_bwd_rows(ring, q, do, bits, T: int, scale: float, samples):
     """dq of the same definition at sampled (b, h, r) query rows only: each row
-    needs just its own kept keys (its softmax, o_r and delta_r).  Returns
+    needs just its own kept keys (its softmax, o_r and delta_r).  The rows of
+    one head are evaluated together, each over its own keep set.  Returns
     dq [n, D] float64."""
     q = np.asarray(q, np.float64)
     do = np.asarray(do, np.float64)
@@ -82,20 +83,23 @@ def sparse_causal_attention_bwd_rows(ring, q, do, bits, T: int, scale: float, sa
     sk = ring.n_live * L
     samples = list(samples)
     out = np.zeros((len(samples), D))
-    cache = {}
+    by_head = {}
     for n, (b, h, r) in enumerate(samples):
-        if (b, h) not in cache:
-            cache = {(b, h): dense_keys(ring, b, h)}
-        K, V = cache[(b, h)]
-        cols = _kept_columns(np.nonzero(bits[b, h, r // T])[0], L, T, nt, sk)
-        if not cols.any():
-            continue
-        Kc, Vc = K[cols], V[cols]
-        s = (Kc @ q[b, r, h]) * scale
-        p = np.exp(s - s.max())
-        p /= p.sum()
-        o = p @ Vc
-        dp = Vc @ do[b, r, h]
-        ds = p * (dp - do[b, r, h] @ o)
-        out[n] = scale * (ds @ Kc)
+        by_head.setdefault((b, h), []).append(n)
+    for (b, h), ns in by_head.items():
+        K, V = dense_keys(ring, b, h)
+        rows = [samples[n][2] for n in ns]
+        M = np.stack([_kept_columns(np.nonzero(bits[b, h, r // T])[0], L, T, nt, sk) for r in rows])
+        Q, dO = q[b, rows, h], do[b, rows, h]
+        S = (Q @ K.T) * scale
+        m = np.max(S, axis=1, where=M, initial=-np.inf)
+        P = np.zeros_like(S)
+        np.exp(S - m[:, None], out=P, where=M)
+        l = P.sum(axis=1, keepdims=True)
+        P /= np.where(l > 0, l, 1.0)
+        O = P @ V
+        dP = dO @ V.T
+        delta = (dO * O).sum(axis=1, keepdims=True)
+        dS = P * (dP - delta)
+        out[ns] = scale * (dS @ K)
     return out

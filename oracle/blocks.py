@@ -1,6 +1,6 @@
 """Oracle of the 3-D block tiling and the structural local mask (test infrastructure only).
 
-What the paper fixes (Sec. 2.3.1, Dynamic Block-Sparse Causal Attention (a);
+What the paper fixes (Sec. 2.3.1, block-sparse causal attention (a);
 App. C): the token grid (t, h, w) of a chunk is divided into non-overlapping
 (b_t, b_h, b_w) blocks, (2, 8, 8) in the paper's model; a spatial locality
 mask confines each block's receptive field to an r x r sliding window of

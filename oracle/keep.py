@@ -1,8 +1,8 @@
 """Oracle of the per-(head, query tile) key-tile keep set (test infrastructure only).
 
-What the paper fixes (Sec. 2.3.1, "Dynamic Block-Sparse Causal Attention",
-Eq. 4): the token grid is split into non-overlapping blocks; each head gets a
-block-level mask that is the intersection of the temporal causal mask (a chunk
+What the paper fixes (Sec. 2.3.1, block-sparse causal attention, Eq. 4): the
+token grid is split into non-overlapping blocks; each head gets a block-level
+mask that is the intersection of the temporal causal mask (a chunk
 attends only to itself and to earlier chunks) with a content-dependent top-k
 keep set; attention is then evaluated over the kept blocks only.
 

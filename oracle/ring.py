@@ -1,10 +1,10 @@
 """Oracle model of the streaming KV cache window (test infrastructure only).
 
 The paper keeps, per attention layer of the single-step SR DiT, a KV cache of
-earlier chunks that the current chunk's queries attend over (App. C: "KV cache:
-3 temporal windows"), and at inference selects a compact cache window
-(Sec. 2.3.2, dynamic cache management (iii); Alg. 3, inference part, "select
-compact SR KV window").  This model realises that window as:
+earlier chunks that the current chunk's queries attend over (App. C gives its
+size, a few chunks), and at inference selects a compact cache window
+(Sec. 2.3.2, dynamic cache management (iii); Alg. 3, inference part, the step
+that picks the SR model's window).  This model realises that window as:
 
 * a list of live chunks in *logical order* = ascending append sequence number;
 * an optional pinned first chunk (the "sink", not named by the paper; it is the

@@ -1,7 +1,7 @@
 """MI355X (gfx950) block-sparse chunk-causal attention over a streaming KV window.
 
 The path of Ultra Flash's single-step SR DiT attention (arXiv 2606.09150,
-Sec. 2.3.1 "Dynamic Block-Sparse Causal Attention", Eq. 4; Sec. 2.3.2 dynamic
+Sec. 2.3.1 (block-sparse causal attention), Eq. 4; Sec. 2.3.2 dynamic
 cache management (iii)), behind the C ABI of ``include/uf.h`` (``libuf.so``):
 
 * ``uf_kv_append`` / ``uf_kv_evict``  -- paged bf16 KV window with a pinned

@@ -11,21 +11,22 @@
 //  * prep: per query tile, Q and dO rows (rows past the chunk end zero),
 //    -LSE/scale (-inf on those rows, so that their weights vanish) and
 //    -delta, which seed the S and dP accumulators;
-//  * dkdv: per window key tile, one workgroup accumulating dK and (a second
-//    launch) one accumulating dV, four waves of 32 keys each; they walk the query tiles whose lists keep
-//    the tile (mask bits) and per 32-query block compute S = Q K^T (keys on the
-//    result lanes), P (and dP = dO V^T, dS), then dV^T += dO^T P or
-//    dK^T += Q^T dS with P or dS used in place as the B operand;
-//  * dq: one workgroup per query tile, four waves of 32 queries; it walks the
-//    row's list and per 32-key block computes S^T = K Q^T, dP^T = V dO^T, dS^T,
-//    then dQ^T += K^T dS^T.
+//  * dkdv: one workgroup of eight waves per window key tile (one per CU).
+//    Waves w and w + 4 share 32 keys.  The workgroup gathers the query tiles
+//    whose mask bit keeps its tile and, per 32-query block, wave w computes
+//    S = Q K^T and P, hands P to wave w + 4 through LDS and accumulates
+//    dV^T += dO^T P, while wave w + 4 computes dP = dO V^T, dS = P (dP - delta)
+//    from the shared P and accumulates dK^T += Q^T dS; the two run one block
+//    apart, and the Q and dO rows of the next query tile are copied while the
+//    current one is used;
+//  * dq: one workgroup of four waves per query tile (two per CU), 32 queries
+//    per wave; it walks the row's list and per 32-key block computes
+//    S^T = K Q^T, dP^T = V dO^T, dS^T, then dQ^T += K^T dS^T.
 // The transposed operands (dO^T, Q^T, K^T, and V rows from the pool's V^T)
 // come from row-major LDS tiles through the transposing LDS read
 // (ds_read_b64_tr_b16), so each tile is copied into LDS once, in the layout the
-// pool or the workspace already holds.  Each workgroup needs at most 73 KB of
-// LDS and 256 registers per lane, so two run on every CU and one's copies
-// overlap the other's products.  No atomics: every output row is owned by one
-// workgroup, so results are reproducible.
+// pool or the workspace already holds.  No atomics: every output row is owned
+// by one workgroup, so results are reproducible.
 #include <type_traits>
 
 #include "attn_common.h"

@@ -2,8 +2,8 @@
 // the window (ring) metadata, and kernel launches.  See include/uf.h for the
 // contract of every entry point.
 //
-// The window realises the paper's compact SR KV cache window (Sec. 2.3.2,
-// dynamic cache management (iii); App. C "KV cache: 3 temporal windows") as a
+// The window realises the paper's compact KV cache window of the SR model
+// (Sec. 2.3.2, dynamic cache management (iii); App. C) as a
 // fixed set of slots in a caller-owned pool: each live chunk occupies one slot;
 // logical order is ascending append sequence number, so an optional pinned
 // first chunk always sits at logical position 0; eviction frees the oldest

@@ -18,12 +18,24 @@ import oracle
 import synth
 
 REL_TOL = 1e-2     # max relative error per row on bf16 O
-# Absolute error on the fp32 log-sum-exp.  The kernel's row sum l adds the
-# bf16-rounded weights (the same values that multiply V), each within a
-# relative 2^-8 of the exact weight, so ln(l) may differ from the exact value
-# by up to ln(1 + 2^-8) = 3.9e-3 when one key dominates the row; the rest of
-# the bar covers fp32 exponent and accumulation rounding.
-LSE_TOL = 5e-3
+# Absolute error on the fp32 log-sum-exp, per tile size (the two kernels sum
+# the row differently).  T = 64: the row sum l adds the bf16-rounded weights
+# (the same values that multiply V), each within a relative 2^-8 of the exact
+# weight, so ln(l) may differ from the exact value by up to ln(1 + 2^-8) =
+# 3.9e-3 when one key dominates the row; the rest of the bar covers fp32
+# exponent and accumulation rounding.  T = 128: l adds the fp32 weights
+# before their rounding, in a few hundred fp32 additions per lane (one per
+# 16-weight partial sum) and a three-way merge, a relative error below
+# 400 * 2^-24 = 2.4e-5; the fp32 scores carry an absolute error of order
+# 2^-24 * D times the largest |scale * q_d k_d| sum, and exp2/log2 one ulp
+# each, so 1e-3 leaves a wide margin and is still four times tighter than the
+# T = 64 bar.
+LSE_TOL_BY_TILE = {64: 5e-3, 128: 1e-3}
+LSE_TOL = max(LSE_TOL_BY_TILE.values())
+
+
+def lse_tol(T):
+    return LSE_TOL_BY_TILE[int(T)]
 
 
 def require_gpu():
@@ -41,6 +53,24 @@ def log(msg):
 
 def f64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def row_errors(g, r):
+    """Per row (last axis = D): max_d|g - r| / max_d|r|; rows whose reference is
+    exactly zero give 0 when g is exactly zero there and inf otherwise."""
+    diff = np.abs(g - r).max(axis=-1)
+    ref = np.abs(r).max(axis=-1)
+    out = np.where(ref > 0, diff / np.where(ref > 0, ref, 1.0), np.where(diff == 0, 0.0, np.inf))
+    return out
+
+
+def head_ring(ring, heads):
+    """The oracle ring restricted to the listed heads (a view: no data copied
+    beyond the fancy index of each chunk)."""
+    sub = oracle.RingModel(ring.max_chunks, ring.pin_sink)
+    sub.next_seq = ring.next_seq
+    sub.live = [oracle.ring.Chunk(c.seq, c.sink, c.k[:, :, heads], c.v[:, :, heads]) for c in ring.live]
+    return sub
 
 
 def row_rel_err(o_gpu, o_ref):

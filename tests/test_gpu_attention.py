@@ -2,10 +2,13 @@
 CPU oracle on the same seeded inputs.
 
 Bar: per (b, h, row) max_d|O_gpu - O_ref| / max_d|O_ref| <= 1e-2 on the bf16
-output, |LSE_gpu - LSE_ref| <= 5e-3.  Full comparison at sizes the oracle
-finishes in seconds (several tiles, ragged tails, T = 64 and 128, batch 2);
-sampled rows at the full workload sizes, in the launch configuration that
-bench.py times; the streaming workload on a fixed head subset.
+output, |LSE_gpu - LSE_ref| <= 5e-3 (64-token tiles) or 1e-3 (128-token
+tiles).  Full comparison at sizes the oracle finishes in seconds (several
+tiles, ragged tails, T = 64 and 128, batch 2) and on the whole tiny and 480p
+windows; at the 1K and 2K windows, in the launch configuration that bench.py
+times, one full head element by element plus one row in every query tile of
+every head; the streaming workload on a fixed head subset at four steps, with
+one of its heads in full at two steps once the window is full.
 """
 
 import math
@@ -16,7 +19,7 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import LSE_TOL, REL_TOL, Case, f64, log, require_gpu, row_rel_err
+from tests.gpu_common import REL_TOL, Case, f64, head_ring, log, lse_tol, require_gpu, row_rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -35,7 +38,7 @@ def _full_check(case, rule, q, scale=None):
     lerr = float(np.abs(lg - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL
-    assert lerr <= LSE_TOL
+    assert lerr <= lse_tol(case.T)
     return o, lse
 
 
@@ -126,9 +129,20 @@ def _sample_rows(rng, L, T, H, per_head):
     return out
 
 
-def _sampled_check(case, rule, q, samples, heads_map=None):
+def _tile_rows(rng, L, T, heads):
+    """One random valid row in every query tile of every listed head."""
+    nt = -(-L // T)
+    out = []
+    for h in heads:
+        for i in range(nt):
+            out.append((0, h, int(i * T + rng.integers(0, min(T, L - i * T)))))
+    return out
+
+
+def _sampled_check(case, rule, q, samples, heads_map=None, o=None, lse=None):
     scale = 1 / math.sqrt(128)
-    o, lse = case.attention(q, scale)
+    if o is None:
+        o, lse = case.attention(q, scale)
     bits = case.oracle_bits(rule)
     hq = case._host(q)
     if heads_map is not None:
@@ -144,29 +158,53 @@ def _sampled_check(case, rule, q, samples, heads_map=None):
     lerr = float(np.abs(gl - LSE).max())
     log(f"  sampled rows={len(samples)} rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL
-    assert lerr <= LSE_TOL
+    assert lerr <= lse_tol(case.T)
     return o, lse
 
 
+def _full_head_check(case, rule, q, o, lse, h, hi=None):
+    """Every row of head h (index hi of the oracle's heads) element by element."""
+    scale = 1 / math.sqrt(128)
+    hi = h if hi is None else hi
+    bits = case.oracle_bits(rule)[:, [h]]
+    ring = head_ring(case.ring, [hi])
+    O, LSE = oracle.sparse_causal_attention(ring, case._host(q)[:, :, [hi]], bits, case.T, scale)
+    og = f64(o[:, :, h:h + 1])
+    lg = f64(lse[:, h:h + 1])
+    err = row_rel_err(og, O)
+    lerr = float(np.abs(lg - LSE).max())
+    log(f"  full head {h}: rows={O.shape[1]} rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL
+    assert lerr <= lse_tol(case.T)
+
+
+FULL_HEAD = {"1k": 7, "2k": 3, "1k_stream": 13}
+
+
 @pytest.mark.parametrize("name", ["1k", "2k"])
-def test_workload_sampled_parity(name):
+def test_workload_full_head_and_every_tile(name):
     P = require_gpu()
-    log(f"attn workload={name} sampled")
+    log(f"attn workload={name}: one full head, one row per query tile of every head")
     wl, case = _workload_case(P, name, "cuda")
     for _ in range(wl.window_chunks):
         case.append()
     rule = case.rule(wl.p_prior)
     counts, _, _ = case.gpu_lists(rule)
-    rng = np.random.default_rng(wl.seed)
-    samples = _sample_rows(rng, wl.chunk_tokens, wl.tile, wl.heads, per_head=10)
-    o, lse = _sampled_check(case, rule, case.query(), samples)
+    q = case.query()
+    o, lse = case.attention(q)
     assert torch.isfinite(o.float()).all() and torch.isfinite(lse).all()
     assert counts.min() >= (1 + int(wl.pin_sink)) * -(-wl.chunk_tokens // wl.tile)
+    rng = np.random.default_rng(wl.seed)
+    samples = _tile_rows(rng, wl.chunk_tokens, wl.tile, range(wl.heads))
+    samples += _sample_rows(rng, wl.chunk_tokens, wl.tile, wl.heads, per_head=2)
+    _sampled_check(case, rule, q, samples, o=o, lse=lse)
+    _full_head_check(case, rule, q, o, lse, FULL_HEAD[name])
 
 
 def test_stream_head_subset_parity():
     P = require_gpu()
     heads = [0, 13, 26, 39]
+    full = FULL_HEAD["1k_stream"]
     wl, case = _workload_case(P, "1k_stream", "cuda", oracle_heads=heads)
     rng = np.random.default_rng(wl.seed)
     for step in range(wl.stream_chunks):
@@ -177,9 +215,13 @@ def test_stream_head_subset_parity():
         q = case.query()
         if step in (0, 3, 4, 11):
             log(f"attn stream step={step}")
-            samples = [(0, i, r) for i, _ in enumerate(heads)
-                       for r in sorted(set([0, 127, 128, wl.chunk_tokens - 1] + list(rng.integers(0, wl.chunk_tokens, 6))))]
-            _sampled_check(case, rule, q, samples, heads_map=heads)
+            o, lse = case.attention(q)
+            samples = _tile_rows(rng, wl.chunk_tokens, wl.tile, range(len(heads)))
+            samples += [(0, i, r) for i, _ in enumerate(heads)
+                        for r in sorted(set([0, 127, 128, wl.chunk_tokens - 1] + list(rng.integers(0, wl.chunk_tokens, 6))))]
+            _sampled_check(case, rule, q, samples, heads_map=heads, o=o, lse=lse)
+            if step in (4, 11):
+                _full_head_check(case, rule, q, o, lse, full, hi=heads.index(full))
         else:
             case.attention(q)
 
@@ -268,7 +310,7 @@ def test_empty_rows_and_stale_entries():
     O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
     fin = np.isfinite(LSE)
     assert row_rel_err(of[:, :, 1:], O[:, :, 1:]) <= REL_TOL
-    assert np.abs(lf[fin] - LSE[fin]).max() <= LSE_TOL
+    assert np.abs(lf[fin] - LSE[fin]).max() <= lse_tol(128)
 
 
 def test_lse_optional_and_outputs_untouched_beyond_shape():
@@ -308,9 +350,9 @@ def test_split_kv_parity(n_split):
     err = row_rel_err(case._host(os_), O)
     lerr = float(np.abs(f64(ls_) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
-    assert err <= REL_TOL and lerr <= LSE_TOL
+    assert err <= REL_TOL and lerr <= lse_tol(128)
     assert row_rel_err(case._host(os_), case._host(o1)) <= REL_TOL
-    assert float((ls_ - l1).abs().max()) <= LSE_TOL
+    assert float((ls_ - l1).abs().max()) <= lse_tol(128)
 
 
 def test_split_kv_more_slices_than_tiles():
@@ -327,7 +369,7 @@ def test_split_kv_more_slices_than_tiles():
     bits = case.oracle_bits(rule)
     O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
     assert row_rel_err(case._host(o), O) <= REL_TOL
-    assert float(np.abs(f64(lse) - LSE).max()) <= LSE_TOL
+    assert float(np.abs(f64(lse) - LSE).max()) <= lse_tol(128)
 
 
 def test_split_kv_480p_full():
@@ -346,4 +388,4 @@ def test_split_kv_480p_full():
     err = row_rel_err(case._host(o), O)
     lerr = float(np.abs(f64(lse) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
-    assert err <= REL_TOL and lerr <= LSE_TOL
+    assert err <= REL_TOL and lerr <= lse_tol(128)

@@ -42,18 +42,20 @@ def _spans_no_tail_clip(kept_tiles, L, T, nt, sk):
 def _make_attend(slip):
     def _attend(Q, K, V, cols, scale):
         n = Q.shape[0]
-        if not cols.any():
-            return np.zeros((n, V.shape[1])), np.full(n, -np.inf), np.zeros(n)
+        M = np.broadcast_to(np.asarray(cols, dtype=bool), (n, K.shape[0]))
         S = (Q @ K.T) * (1.0 if slip == "scale" else scale)
-        S[:, ~cols] = -np.inf
-        m = S.max(axis=1)
-        P = np.exp(-(S - m[:, None])) if slip == "sign" else np.exp(S - m[:, None])
+        m = np.max(S, axis=1, where=M, initial=-np.inf)
+        P = np.zeros_like(S)
         if slip == "sign":
-            P[:, ~cols] = 0.0
+            np.exp(-(S - m[:, None]), out=P, where=M)
+        else:
+            np.exp(S - m[:, None], out=P, where=M)
         l = P.sum(axis=1)
-        O = (P @ (K if slip == "operand" else V)) / l[:, None]
-        lse = np.log(l) if slip == "lse" else m + np.log(l)
-        return O, lse, (P / l[:, None]).sum(axis=1)
+        has = l > 0
+        ls = np.where(has, l, 1.0)
+        O = (P @ (K if slip == "operand" else V)) / ls[:, None]
+        lse = np.where(has, (0.0 if slip == "lse" else m) + np.log(ls), -np.inf)
+        return O, lse, (P / ls[:, None]).sum(axis=1)
     return _attend
 
 
