@@ -68,7 +68,11 @@ from .blocks import (
     attention_in_raster_bwd,
 )
 from .mask import block_sparse_mask
-from .backward import sparse_causal_attention_bwd, sparse_causal_attention_bwd_rows
+from .backward import (
+    sparse_causal_attention_bwd,
+    sparse_causal_attention_bwd_rows,
+    sparse_causal_attention_bwd_scales,
+)
 from .attention import (
     sparse_causal_attention,
     sparse_causal_attention_rows,
@@ -103,6 +107,7 @@ __all__ = [
     "topk_bits",
     "sparse_causal_attention_bwd",
     "sparse_causal_attention_bwd_rows",
+    "sparse_causal_attention_bwd_scales",
     "sparse_causal_attention",
     "sparse_causal_attention_rows",
     "dense_keys",

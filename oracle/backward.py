@@ -71,6 +71,61 @@ def sparse_causal_attention_bwd(ring, q, do, bits, T: int, scale: float, heads=N
     return dq, dk, dv
 
 
+def sparse_causal_attention_bwd_scales(ring, q, do, bits, T: int, scale: float, heads=None):
+    """Scale of the summands of every gradient element (float64), for error bars.
+
+    Each gradient element is a sum over keys (dq) or query rows (dk, dv) of
+    products of the definition's factors.  Bounding each factor by its
+    magnitude, with ds_rc = p_rc (dp_rc - delta_r) bounded by
+    m_rc = p_rc (|dp_rc - delta_r| + sum_d |do_rd o_rd|) -- the second term is
+    the size of delta's own terms, so that a relative error in those terms is
+    covered where dp_rc - delta_r cancels (a near one-hot row) --, the scale of
+    an element is the root sum of squares of its summands' bounds:
+
+        sdq_rd = scale * sqrt(sum_c m_rc^2 k_cd^2)
+        sdk_cd = scale * sqrt(sum_r m_rc^2 q_rd^2)
+        sdv_cd =         sqrt(sum_r p_rc^2 do_rd^2)
+
+    Independent relative errors of size u in the factors change an element by
+    about u times its scale.  Same shapes and head selection as
+    ``sparse_causal_attention_bwd``.
+    """
+    chunks = ring.logical_chunks()
+    B, L, H, D = q.shape
+    n_live = len(chunks)
+    nt, _ = tile_geometry(L, T)
+    sk = L * n_live
+    sq = np.zeros((B, L, H, D))
+    sk2 = np.zeros((n_live, B, L, H, D))
+    sv2 = np.zeros((n_live, B, L, H, D))
+    for b in range(B):
+        for h in (range(H) if heads is None else heads):
+            K, V = dense_keys(ring, b, h)
+            aK = np.zeros((sk, D))
+            aV = np.zeros((sk, D))
+            for i in range(nt):
+                r0, r1 = i * T, min((i + 1) * T, L)
+                cols = _kept_columns(np.nonzero(bits[b, h, i])[0], L, T, nt, sk)
+                if not cols.any():
+                    continue
+                Q = q[b, r0:r1, h].astype(np.float64)
+                dO = do[b, r0:r1, h].astype(np.float64)
+                Kc, Vc = K[cols], V[cols]
+                S = (Q @ Kc.T) * scale
+                P = np.exp(S - S.max(axis=1, keepdims=True))
+                P /= P.sum(axis=1, keepdims=True)
+                O = P @ Vc
+                dP = dO @ Vc.T
+                delta = (dO * O).sum(axis=1, keepdims=True)
+                M2 = (P * (np.abs(dP - delta) + np.abs(dO * O).sum(axis=1, keepdims=True))) ** 2
+                sq[b, r0:r1, h] = scale * np.sqrt(M2 @ (Kc * Kc))
+                aK[cols] += scale * scale * (M2.T @ (Q * Q))
+                aV[cols] += (P * P).T @ (dO * dO)
+            sk2[:, b, :, h] = aK.reshape(n_live, L, D)
+            sv2[:, b, :, h] = aV.reshape(n_live, L, D)
+    return sq, np.sqrt(sk2), np.sqrt(sv2)
+
+
 def sparse_causal_attention_bwd_rows(ring, q, do, bits, T: int, scale: float, samples):
     """dq of the same definition at sampled (b, h, r) query rows only: each row
     needs just its own kept keys (its softmax, o_r and delta_r).  The rows of

@@ -64,6 +64,15 @@ def row_errors(g, r):
     return out
 
 
+def row_errors_scaled(g, r, sc):
+    """Per row: max_d|g - r| / max(max_d|r|, max_d sc), sc the oracle's summand
+    scales of the same elements (for rows where the exact sum cancels);
+    a row with zero reference and zero scale must be exactly zero."""
+    diff = np.abs(g - r).max(axis=-1)
+    den = np.maximum(np.abs(r).max(axis=-1), sc.max(axis=-1))
+    return np.where(den > 0, diff / np.where(den > 0, den, 1.0), np.where(diff == 0, 0.0, np.inf))
+
+
 def head_ring(ring, heads):
     """The oracle ring restricted to the listed heads (a view: no data copied
     beyond the fancy index of each chunk)."""

@@ -26,7 +26,7 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import Case, f64, head_ring, log, require_gpu, row_errors
+from tests.gpu_common import Case, f64, head_ring, log, require_gpu, row_errors, row_errors_scaled
 
 pytestmark = pytest.mark.gpu
 
@@ -105,13 +105,35 @@ def test_small_backward_parity(B, L, H, mc, pin, n, p):
 
 
 def test_backward_large_logits():
-    """Peaked rows (q and k scaled by 3): P near one-hot, delta near dP."""
+    """Peaked rows (q and k scaled by 3): P near one-hot, so dP - delta cancels
+    for the dominant key and the exact dQ and dK rows of such queries shrink
+    towards zero while the rounding of the kernel's factors (delta from the
+    bf16 O, P and dS in bf16) does not.  Bar: per row, max_d|diff| over the
+    larger of max_d|ref| and the largest scale of the row's summands
+    (oracle.sparse_causal_attention_bwd_scales) <= 1e-2; the plain per-row
+    form must still hold for dV, which has no such cancellation."""
     P = require_gpu()
     log("bwd large logits")
     case = Case(P, 1, 500, 2, 128, 4, True, seed=2101, gain=lambda c, n: 3.0 if n in ("q", "k") else 1.0)
     for _ in range(4):
         case.append()
-    _full_compare(case, case.rule(0.5))
+    rule = case.rule(0.5)
+    scale = 1 / math.sqrt(128)
+    q, o, lse, do, dq, dk, dv = _run(case, rule, scale)
+    bits = case.oracle_bits(rule)
+    hq, hdo = case._host(q), case._host(do)
+    rq, rk, rv = oracle.sparse_causal_attention_bwd(case.ring, hq, hdo, bits, case.T, scale)
+    sq, sk, sv = oracle.sparse_causal_attention_bwd_scales(case.ring, hq, hdo, bits, case.T, scale)
+    gq, gk, gv = dq.cpu().numpy(), dk.cpu().numpy(), dv.cpu().numpy()
+    worst = {"dq": 0.0, "dk": 0.0, "dv": 0.0, "dv_plain": 0.0, "dq_plain": 0.0}
+    for h in range(case.H):
+        worst["dq"] = max(worst["dq"], float(row_errors_scaled(gq[0, :, h], rq[0, :, h], sq[0, :, h]).max()))
+        worst["dk"] = max(worst["dk"], float(row_errors_scaled(gk[:, 0, :, h], rk[:, 0, :, h], sk[:, 0, :, h]).max()))
+        worst["dv"] = max(worst["dv"], float(row_errors_scaled(gv[:, 0, :, h], rv[:, 0, :, h], sv[:, 0, :, h]).max()))
+        worst["dv_plain"] = max(worst["dv_plain"], _rows(gv[:, 0, :, h], rv[:, 0, :, h]))
+        worst["dq_plain"] = max(worst["dq_plain"], _rows(gq[0, :, h], rq[0, :, h]))
+    log("  " + " ".join(f"{k}={v:.3e}" for k, v in worst.items()))
+    assert max(worst["dq"], worst["dk"], worst["dv"], worst["dv_plain"]) <= GRAD_TOL, worst
 
 
 def test_backward_poisoned_padding_and_determinism():

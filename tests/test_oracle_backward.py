@@ -140,3 +140,103 @@ def test_sampled_rows_match_full_backward():
     want = np.stack([dq[b, r, h] for b, h, r in samples])
     assert np.allclose(got, want, atol=1e-12)
     assert np.all(got[3] == 0)
+
+
+def _brute_scales(ring, q, do, bits, T, scale):
+    """Element-by-element loops over the definition of the summand scales."""
+    chunks = ring.logical_chunks()
+    B, L, H, D = q.shape
+    nt = -(-L // T)
+    keys = [(p, t) for p in range(len(chunks)) for t in range(L)]
+    sq = np.zeros_like(q)
+    sk = np.zeros((len(chunks), B, L, H, D))
+    sv = np.zeros_like(sk)
+    for b in range(B):
+        for h in range(H):
+            for r in range(L):
+                kept = [(p, t) for (p, t) in keys if bits[b, h, r // T, p * nt + t // T]]
+                s = [scale * sum(q[b, r, h, d] * chunks[p].k[b, t, h, d] for d in range(D)) for p, t in kept]
+                mx = max(s)
+                e = [np.exp(x - mx) for x in s]
+                pr = [x / sum(e) for x in e]
+                o = [sum(pr[n] * chunks[p].v[b, t, h, d] for n, (p, t) in enumerate(kept)) for d in range(D)]
+                dp = [sum(do[b, r, h, d] * chunks[p].v[b, t, h, d] for d in range(D)) for p, t in kept]
+                delta = sum(do[b, r, h, d] * o[d] for d in range(D))
+                dsum = sum(abs(do[b, r, h, d] * o[d]) for d in range(D))
+                for n, (p, t) in enumerate(kept):
+                    m = pr[n] * (abs(dp[n] - delta) + dsum)
+                    for d in range(D):
+                        sq[b, r, h, d] += (scale * m * chunks[p].k[b, t, h, d]) ** 2
+                        sk[p, b, t, h, d] += (scale * m * q[b, r, h, d]) ** 2
+                        sv[p, b, t, h, d] += (pr[n] * do[b, r, h, d]) ** 2
+    return np.sqrt(sq), np.sqrt(sk), np.sqrt(sv)
+
+
+def test_summand_scales_brute_force():
+    B, L, H, D, T = 1, 5, 2, 3, 2
+    ring, q, do, rng = _ring(B, L, H, D, 3, True, 11)
+    bits = _bits(rng, B, H, 3, 9)
+    got = oracle.sparse_causal_attention_bwd_scales(ring, q, do, bits, T, 0.6)
+    want = _brute_scales(ring, q, do, bits, T, 0.6)
+    for g, w in zip(got, want):
+        assert np.allclose(g, w, rtol=1e-12, atol=1e-14)
+
+
+def test_summand_scales_single_key_closed_form():
+    """One kept key: p = 1 and o = v, so dp - delta = 0 and the exact dq and dk
+    vanish, while the scales keep the size of delta's terms."""
+    rng = np.random.default_rng(12)
+    ring = oracle.RingModel(1, False)
+    k, v = rng.standard_normal((1, 1, 1, 4)), rng.standard_normal((1, 1, 1, 4))
+    ring.append(k, v)
+    q, do = rng.standard_normal((1, 1, 1, 4)), rng.standard_normal((1, 1, 1, 4))
+    bits = np.ones((1, 1, 1, 1), bool)
+    dq, dk, dv = oracle.sparse_causal_attention_bwd(ring, q, do, bits, 1, 0.5)
+    sq, sk, sv = oracle.sparse_causal_attention_bwd_scales(ring, q, do, bits, 1, 0.5)
+    assert np.allclose(dq, 0, atol=1e-15) and np.allclose(dk, 0, atol=1e-15)
+    assert np.allclose(dv[0], do)
+    dsum = np.abs(do * v).sum()
+    assert np.allclose(sq[0, 0, 0], 0.5 * dsum * np.abs(k[0, 0, 0]))
+    assert np.allclose(sk[0, 0, 0, 0], 0.5 * dsum * np.abs(q[0, 0, 0]))
+    assert np.allclose(sv[0, 0, 0, 0], np.abs(do[0, 0, 0]))
+
+
+def test_summand_scales_bound_perturbed_factors():
+    """Relative perturbations of size u in p, in dp - delta's factors and in
+    delta's terms move every gradient element by a few u times its scale."""
+    B, L, H, D, T = 1, 40, 1, 16, 8
+    ring, q, do, rng = _ring(B, L, H, D, 3, True, 13)
+    for c in ring.live:          # peaked rows
+        c.k *= 3.0
+    q = q * 3.0
+    bits = _bits(rng, B, H, 5, 15)
+    scale, u = 0.5, 1e-3
+    sq, sk, sv = oracle.sparse_causal_attention_bwd_scales(ring, q, do, bits, T, scale)
+    K = np.concatenate([c.k[0, :, 0] for c in ring.logical_chunks()])
+    V = np.concatenate([c.v[0, :, 0] for c in ring.logical_chunks()])
+    cols = np.zeros((5, 15 * T), bool)
+    for i in range(5):
+        for j in np.nonzero(bits[0, 0, i])[0]:
+            p, t = divmod(j, 5)
+            cols[i, p * L + t * T:p * L + t * T + T] = True
+    exact = np.zeros((L, D)), np.zeros((3 * L, D)), np.zeros((3 * L, D))
+    pert = np.zeros((L, D)), np.zeros((3 * L, D)), np.zeros((3 * L, D))
+    for i in range(5):
+        rows = slice(i * T, (i + 1) * T)
+        c = cols[i]
+        Qi, dOi = q[0, rows, 0], do[0, rows, 0]
+        S = Qi @ K[c].T * scale
+        P = np.exp(S - S.max(1, keepdims=True))
+        P /= P.sum(1, keepdims=True)
+        O = P @ V[c]
+        for out, noisy in ((exact, False), (pert, True)):
+            e = (lambda shape: 1 + u * rng.uniform(-1, 1, shape)) if noisy else (lambda shape: 1.0)
+            Pn = P * e(P.shape)
+            delta = (dOi * O * e(O.shape)).sum(1, keepdims=True)
+            dS = Pn * (dOi @ V[c].T - delta) * e(P.shape)
+            out[0][rows] += scale * dS @ K[c]
+            out[1][c] += scale * dS.T @ Qi
+            out[2][c] += Pn.T @ dOi
+    for g, x, s_ in ((pert[0], exact[0], sq[0, :, 0]), (pert[1], exact[1], np.concatenate(sk[:, 0, :, 0])),
+                     (pert[2], exact[2], np.concatenate(sv[:, 0, :, 0]))):
+        assert np.all(np.abs(g - x) <= 6 * u * s_ + 1e-15)
