@@ -326,6 +326,27 @@ int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o,
                               const float* d_lse, const void* d_lists, float scale, float* d_dq,
                               float* d_dk, float* d_dv, void* d_work, size_t work_bytes, void* stream);
 
+/* No-allocation backward, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving or training loops, harnesses
+ * that forbid allocation): the same operation, arguments, outputs and errors
+ * as uf_sparse_causal_attn_bwd, without the workspace.  Its query-tile
+ * records (the 66,560 bytes per list row that uf_attn_bwd_work_bytes counts)
+ * live in a device array inside the library, UF_BWD_SCRATCH_BYTES on every GPU
+ * it runs on, held from the first call on that GPU until the process ends.
+ * Needs B*H*NT*66560 <= UF_BWD_SCRATCH_BYTES, i.e. at most 1,008 list rows
+ * (query tiles over all heads), else UF_ERR_CAPACITY.  Every call on one GPU
+ * uses the same array and leaves the last call's records in it (each call
+ * rewrites every record it reads first, so nothing needs clearing): calls that
+ * overlap in time on one GPU (other streams, or other threads without
+ * ordering) race and give wrong results; calls ordered on one stream are safe.
+ * The first call on a GPU looks the array's address up (no allocation); no
+ * call allocates or frees device or pinned memory.  Errors: as
+ * uf_sparse_causal_attn_bwd, plus UF_ERR_CAPACITY. */
+#define UF_BWD_SCRATCH_BYTES ((size_t)64 << 20)
+int uf_sparse_causal_attn_bwd_noalloc(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
+                                      const float* d_lse, const void* d_lists, float scale, float* d_dq,
+                                      float* d_dk, float* d_dv, void* stream);
+
 /* Static text of a status code. */
 const char* uf_status_string(int status);
 

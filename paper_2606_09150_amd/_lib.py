@@ -93,6 +93,7 @@ _SIGNATURES = {
     "uf_attn_bwd_work_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "uf_sparse_causal_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P,
                                                  ctypes.c_size_t, _P]),
+    "uf_sparse_causal_attn_bwd_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P]),
     "uf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "uf_last_error": (ctypes.c_char_p, []),
 }
@@ -269,6 +270,12 @@ def uf_sparse_causal_attn_bwd(handle, q, o, do, lse, lists, scale: float, dq, dk
     s = None if q is None else _stream_ptr(stream)
     _check(load().uf_sparse_causal_attn_bwd(handle, _ptr(q), _ptr(o), _ptr(do), _ptr(lse), _ptr(lists),
                                             ctypes.c_float(scale), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(work), n, s))
+
+
+def uf_sparse_causal_attn_bwd_noalloc(handle, q, o, do, lse, lists, scale: float, dq, dk, dv, stream=None) -> None:
+    s = None if q is None else _stream_ptr(stream)
+    _check(load().uf_sparse_causal_attn_bwd_noalloc(handle, _ptr(q), _ptr(o), _ptr(do), _ptr(lse), _ptr(lists),
+                                                    ctypes.c_float(scale), _ptr(dq), _ptr(dk), _ptr(dv), s))
 
 
 def uf_status_string(status: int) -> str:

@@ -27,6 +27,7 @@
 // (ds_read_b64_tr_b16), so each tile is copied into LDS once, in the layout the
 // pool or the workspace already holds.  No atomics: every output row is owned
 // by one workgroup, so results are reproducible.
+#include <mutex>
 #include <type_traits>
 
 #include "attn_common.h"
@@ -547,6 +548,56 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
 }
 
 }  // namespace
+
+// Scratch of the no-allocation backward: the query-tile records that
+// launch_attn_bwd keeps in the caller's workspace, in a file-scope device
+// array instead.  Every GPU the library runs on holds its own copy until the
+// process ends; in host code the array's name is only a stand-in, so kernels
+// are handed its device address, looked up once per device.
+static __device__ __align__(256) uint8_t scratch[kBwdScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device of `stream` (the current device
+// for the null stream), looked up with that device current on the first call.
+hipError_t scratch_address(hipStream_t stream, void** out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  int dev = cur;
+  if (stream != nullptr && (e = hipStreamGetDevice(stream, &dev)) != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t r = hipSetDevice(cur);
+      if (e == hipSuccess) e = r;
+    }
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd_noalloc(BwdArgs a, hipStream_t stream) {
+  if (size_t(a.B) * size_t(a.H) * size_t(a.NT) * kBwdQTile > kBwdScratchBytes) return hipErrorInvalidValue;
+  void* p = nullptr;
+  hipError_t e = scratch_address(stream, &p);
+  if (e != hipSuccess) return e;
+  a.work = static_cast<uint8_t*>(p);
+  return launch_attn_bwd(a, stream);
+}
 
 hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream) {
   const unsigned qrows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);

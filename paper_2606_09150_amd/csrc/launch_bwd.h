@@ -29,5 +29,11 @@ struct BwdArgs {
   TileValid tv;
 };
 hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream);
+// The same launches with the query-tile records in the library's own device
+// scratch (kBwdScratchBytes per GPU) instead of a.work; needs
+// B*H*NT*kBwdQTile <= kBwdScratchBytes (hipErrorInvalidValue otherwise).
+// Allocates nothing; calls that overlap on one GPU race.
+constexpr size_t kBwdScratchBytes = UF_BWD_SCRATCH_BYTES;
+hipError_t launch_attn_bwd_noalloc(BwdArgs a, hipStream_t stream);
 
 }  // namespace uf

@@ -485,9 +485,13 @@ int uf_attn_bwd_work_bytes(const uf_kv* kv, size_t* bytes) {
   return ok();
 }
 
-int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
-                              const float* d_lse, const void* d_lists, float scale, float* d_dq, float* d_dk,
-                              float* d_dv, void* d_work, size_t work_bytes, void* stream) {
+namespace {
+
+// Validation and kernel arguments shared by both backward entry points; the
+// caller's workspace is checked (and set) only when `work` is true.
+int bwd_args(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do, const float* d_lse,
+             const void* d_lists, float scale, float* d_dq, float* d_dk, float* d_dv, bool work, void* d_work,
+             size_t work_bytes, uf::BwdArgs* out) {
   if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
   if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "the backward needs 128-token tiles");
   if (kv->nt > uf::kBwdMaxQTiles) return fail(UF_ERR_UNSUPPORTED, "the backward handles at most %d query tiles", uf::kBwdMaxQTiles);
@@ -498,12 +502,14 @@ int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o,
     return fail(UF_ERR_ARG, "do, lse, dq, dk or dv is null");
   if (!aligned(d_do, 16) || !aligned(d_dq, 16) || !aligned(d_dk, 16) || !aligned(d_dv, 16))
     return fail(UF_ERR_ARG, "do, dq, dk and dv must be 16-byte aligned");
-  if (d_work == nullptr || !aligned(d_work, 16)) return fail(UF_ERR_ARG, "work must be non-null and 16-byte aligned");
-  if (work_bytes < bwd_work_bytes(kv))
-    return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, bwd_work_bytes(kv));
+  if (work) {
+    if (d_work == nullptr || !aligned(d_work, 16)) return fail(UF_ERR_ARG, "work must be non-null and 16-byte aligned");
+    if (work_bytes < bwd_work_bytes(kv))
+      return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, bwd_work_bytes(kv));
+  }
   const uf_lists_layout lay = kv->layout();
   if (int64_t(lay.rows) * int64_t(kv->live.size()) > INT32_MAX) return fail(UF_ERR_ARG, "shape too large");
-  uf::BwdArgs a{};
+  uf::BwdArgs& a = *out;
   a.q = f.q;
   a.o = f.o;
   a.dout = static_cast<const uint16_t*>(d_do);
@@ -530,8 +536,36 @@ int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o,
   a.scale_log2 = f.scale_log2;
   for (int p = 0; p < a.n_live; ++p) a.slot_of[p] = f.slot_of[p];
   a.tv = f.tv;
+  return ok();
+}
+
+}  // namespace
+
+int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
+                              const float* d_lse, const void* d_lists, float scale, float* d_dq, float* d_dk,
+                              float* d_dv, void* d_work, size_t work_bytes, void* stream) {
+  uf::BwdArgs a{};
+  if (int s = bwd_args(kv, d_q, d_o, d_do, d_lse, d_lists, scale, d_dq, d_dk, d_dv, true, d_work, work_bytes, &a))
+    return s;
+  if (kv->dry()) return ok();
   hipError_t e = uf::launch_attn_bwd(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_bwd launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_sparse_causal_attn_bwd_noalloc(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
+                                      const float* d_lse, const void* d_lists, float scale, float* d_dq,
+                                      float* d_dk, float* d_dv, void* stream) {
+  if (kv != nullptr && kv->d.tile == 128 && bwd_work_bytes(kv) > uf::kBwdScratchBytes)
+    return fail(UF_ERR_CAPACITY, "the backward of %d list rows needs %zu bytes of scratch, the library holds %zu "
+                "(at most %zu rows)", kv->layout().rows, bwd_work_bytes(kv), uf::kBwdScratchBytes,
+                uf::kBwdScratchBytes / uf::kBwdQTile);
+  uf::BwdArgs a{};
+  if (int s = bwd_args(kv, d_q, d_o, d_do, d_lse, d_lists, scale, d_dq, d_dk, d_dv, false, nullptr, 0, &a))
+    return s;
+  if (kv->dry()) return ok();
+  hipError_t e = uf::launch_attn_bwd_noalloc(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_bwd (no-allocation) launch: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -34,7 +34,7 @@ def _declared():
 def test_library_exports_every_declared_symbol(P):
     from paper_2606_09150_amd import _lib
     names = _declared()
-    assert len(names) == 23
+    assert len(names) == 24
     lib = ctypes.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -277,3 +277,20 @@ def test_backward_host_paths(P):
     w64.append(None, None)
     assert status(L.uf_attn_bwd_work_bytes, w64.handle) == L.UF_ERR_UNSUPPORTED
     assert status(bwd, w64.handle, *args) == L.UF_ERR_UNSUPPORTED
+
+    # the no-allocation variant: same checks, no workspace, and a capacity
+    # limit of its own scratch (66,560 bytes per list row, 64 MiB in all)
+    na = L.uf_sparse_causal_attn_bwd_noalloc
+    nargs = (None, None, None, None, None, 0.1, None, None, None)
+    wn = _dry(P, max_chunks=4, L=300, T=128, H=2)
+    assert status(na, wn.handle, *nargs) == L.UF_ERR_EMPTY
+    wn.append(None, None)
+    na(wn.handle, *nargs)                                                  # dry run: no device work
+    assert status(na, w64.handle, *nargs) == L.UF_ERR_UNSUPPORTED
+    fits = _dry(P, max_chunks=2, L=1008 * 128, T=128, H=1)               # 1,008 rows: exactly the scratch
+    fits.append(None, None)
+    na(fits.handle, *nargs)
+    big = _dry(P, max_chunks=2, L=24480, T=128, H=12)                    # the 1K window: 2,304 rows
+    big.append(None, None)
+    assert status(na, big.handle, *nargs) == L.UF_ERR_CAPACITY
+    assert "1008 rows" in L.uf_last_error()
