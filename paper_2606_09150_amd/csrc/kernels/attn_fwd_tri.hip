@@ -70,6 +70,7 @@ constexpr uint32_t kHalf = 16384;      // bytes of a half-tile buffer
 constexpr int kGroupBytes = 3 * kHalf;
 constexpr int kBuffers = 9;
 constexpr float kSumBound = 4096.0f;   // lane row-sum bound of one half unit's 16 weights
+constexpr int kUnitCap = 4095;         // non-empty units of a row listed in LDS (blocked windows)
 
 // 3-bit XOR pattern of LDS row r (r % 16): bijective in bits 0..2 for either
 // value of bit 3, and in bits 1..3 for either value of bit 0.
@@ -286,9 +287,14 @@ __device__ __forceinline__ void tri_second(TriState& st, float c2, const HalfCop
 // SPLIT: workgroup (row, s) of a split-KV launch takes list entries
 // [s*count/split, (s+1)*count/split) of its row and writes its unnormalised
 // partial (O relative to its offset m, and l) to a.work; a merge combines them.
-template <bool SPLIT>
+// UNITS (windows with block geometry, whose tiles often hold 64 tokens or
+// fewer): the workgroup first lists its row's units that hold a valid key
+// (tile j and key half, in list order) in LDS and walks only those, so a key
+// half without a valid token costs neither copies nor products.
+template <bool SPLIT, bool UNITS>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   __shared__ uint4 sbuf[kBuffers][kHalf / 16];
+  __shared__ uint32_t sunit[UNITS ? kUnitCap + 1 : 1];   // (j << 1) | key half; the count last
 
   const int row = SPLIT ? int(blockIdx.x) / a.split : int(blockIdx.x);
   const int part = SPLIT ? int(blockIdx.x) - row * a.split : 0;
@@ -337,9 +343,38 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   const int first = SPLIT ? int(int64_t(part) * total / a.split) : 0;
   const int count = SPLIT ? int(int64_t(part + 1) * total / a.split) - first : total;
   const float c2 = a.scale_log2;
-  const int U = 2 * count;            // units
-  const int P = U + 3;                // phases
   const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap + first;
+  int U = 2 * count;                  // units
+  if constexpr (UNITS) {
+    // non-empty units of the row's slice, in list order; entries naming a
+    // tile outside the window count no key and give none
+    if (wave == 0) {
+      const int32_t* lv = a.idx + size_t(row) * a.nk_cap + first;
+      int off = 0;
+      for (int base = 0; base < count; base += 64) {
+        const int e = base + lane;
+        int n = 0;
+        uint32_t j = 0;
+        if (e < count) {
+          j = uint32_t(lv[e]);
+          if (j < uint32_t(a.nk)) {
+            const int v = tile_valid(a.tv, int(j % uint32_t(a.NT)), a.NT, a.tail, kT);
+            n = (v > 64) ? 2 : (v > 0 ? 1 : 0);
+          }
+        }
+        const uint64_t b1 = __ballot(n >= 1), b2 = __ballot(n == 2);
+        const uint64_t below = (uint64_t(1) << lane) - 1;
+        const int pos = off + __popcll(b1 & below) + __popcll(b2 & below);
+        if (n >= 1) sunit[pos] = j << 1;
+        if (n == 2) sunit[pos + 1] = (j << 1) | 1u;
+        off += __popcll(b1) + __popcll(b2);
+      }
+      if (lane == 0) sunit[kUnitCap] = uint32_t(off);
+    }
+    __syncthreads();
+    U = int(__builtin_amdgcn_readfirstlane(sunit[kUnitCap]));
+  }
+  const int P = U + 3;                // phases
 
   // Page and valid keys of unit w (tile w/2, key half w%2).  An entry naming
   // a tile outside the window (stale lists) reads a page of this head and
@@ -347,11 +382,21 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   struct Unit {
     const uint8_t* page;
     int valid;
+    int half;         // key half of the tile (UNITS; otherwise w % 2)
   };
   auto unit = [&](int w) {
-    Unit r{head_pages, 0};
+    Unit r{head_pages, 0, 0};
     if (w >= U) return r;
-    const int j = list[w >> 1];
+    int j, half;
+    if constexpr (UNITS) {
+      const uint32_t x = __builtin_amdgcn_readfirstlane(sunit[w]);
+      j = int(x >> 1);
+      half = int(x & 1u);
+    } else {
+      j = list[w >> 1];
+      half = w & 1;
+    }
+    r.half = half;
     if (unsigned(j) >= unsigned(a.nk)) {
       r.page = head_pages + size_t(a.slot_of[0]) * slot_stride;
       return r;
@@ -359,17 +404,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
     const int pos = div_nt(uint32_t(j), a.nt_div);
     const int t = j - pos * a.NT;
     r.page = head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
-    r.valid = min(max(tile_valid(a.tv, t, a.NT, a.tail, kT) - 64 * (w & 1), 0), 64);
+    r.valid = min(max(tile_valid(a.tv, t, a.NT, a.tail, kT) - 64 * half, 0), 64);
     return r;
   };
   // page bytes: K block j (dimensions 64j..) at 16384 j, rows of 128 bytes;
   // V^T block j (keys 64j..) at 32768 + 16384 j.  Copy c of a half: K rows
   // 64(w%2) + 8(c%8) .. of block c/8; V^T rows 8(c%8) + 64(c/8) .. of block w%2.
   auto kcopy = [&](const Unit& un, int w, int kbuf) {
-    return HalfCopy{un.page + 8192 * (w & 1) + 1024 * qw, lds_base + uint32_t(kbuf) * kHalf, 16384u, w < U};
+    const int half = UNITS ? un.half : (w & 1);
+    return HalfCopy{un.page + 8192 * half + 1024 * qw, lds_base + uint32_t(kbuf) * kHalf, 16384u, w < U};
   };
   auto vcopy = [&](const Unit& un, int w, int vbuf) {
-    return HalfCopy{un.page + 32768 + 16384 * (w & 1) + 1024 * qw, lds_base + uint32_t(vbuf) * kHalf, 8192u, w < U};
+    const int half = UNITS ? un.half : (w & 1);
+    return HalfCopy{un.page + 32768 + 16384 * half + 1024 * qw, lds_base + uint32_t(vbuf) * kHalf, 8192u, w < U};
   };
   auto issue = [&](const HalfCopy& cp) {
     if (cp.on)
@@ -601,15 +648,24 @@ __global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
 
 }  // namespace
 
+// The unit table holds every unit of a row when 2 * nk_cap <= kUnitCap.
+inline bool use_units(const AttnArgs& a) { return a.tv.blocked && 2 * a.nk_cap <= kUnitCap; }
+
 hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
-  attn_fwd_tri_kernel<false><<<blocks, kThreads, 0, stream>>>(a);
+  if (use_units(a))
+    attn_fwd_tri_kernel<false, true><<<blocks, kThreads, 0, stream>>>(a);
+  else
+    attn_fwd_tri_kernel<false, false><<<blocks, kThreads, 0, stream>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT) * unsigned(a.split);
-  attn_fwd_tri_kernel<true><<<blocks, kThreads, 0, stream>>>(a);
+  if (use_units(a))
+    attn_fwd_tri_kernel<true, true><<<blocks, kThreads, 0, stream>>>(a);
+  else
+    attn_fwd_tri_kernel<true, false><<<blocks, kThreads, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_attn_split_merge(a, stream);

@@ -182,6 +182,31 @@ G128 = oracle.BlockGeom(3, 10, 12, 2, 8, 8)     # 8 blocks of 128 (the backward 
 
 
 @pytest.mark.parametrize("r", [0, 1])
+def test_blocked_128_attention_skips_empty_key_halves(r):
+    """128-token blocks (valid counts 128, 64, 32, 16 at the first block time and
+    64, 32, 16, 8 at the second): the attention walks only the 64-key units that
+    hold a valid key; against the oracle in raster order, whole and split."""
+    P = require_gpu()
+    log(f"blocks 128 attention r={r}")
+    case = BlockCase(P, G128, 2, 2, 4, True, seed=51)
+    for _ in range(5):
+        case.append()
+    case.win.build_lists(case.seed, 0.5, local_r=r)
+    bits = case.oracle_bernoulli(0.5, r)
+    case.compare_lists(bits)
+    q = case.draw(96, "q")
+    case.check_attention(q, bits)
+    qb = _permute(P, G128, q, 0)
+    o1, l1 = case.win.attention(qb)
+    o3, l3 = case.win.attention(qb, split=3)
+    torch.cuda.synchronize()
+    src = oracle.block_order(G128)
+    valid = torch.from_numpy(src >= 0).cuda()
+    assert row_rel_err(f64(o3[:, valid]), f64(o1[:, valid])) <= REL_TOL
+    assert float((l3[:, :, valid] - l1[:, :, valid]).abs().max()) <= lse_tol(128)
+
+
+@pytest.mark.parametrize("r", [0, 1])
 def test_blocked_backward(r):
     """dQ, dK, dV on block-ordered tokens (uf_sparse_causal_attn_bwd with block
     geometry) mapped back to raster order, against the oracle's raster-order
