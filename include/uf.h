@@ -305,6 +305,31 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
                                     void* d_o, float* d_lse, int32_t n_split, void* d_work,
                                     size_t work_bytes, void* stream);
 
+/* Split-KV of the rows of the last, partly filled round only.  With one
+ * workgroup per compute unit a window of R rows runs in ceil(R / n_cu) rounds;
+ * when the last round is partly empty (444 rows on 256 CUs: the second round
+ * leaves 68 CUs idle), cutting only its rows into slices that fill the
+ * compute units shortens the launch.  uf_sparse_causal_attn_fwd_split_rows
+ * runs rows 0 .. split_from-1 whole and cuts every later row into n_split
+ * slices as uf_sparse_causal_attn_fwd_split does (split_from = 0: every row,
+ * which is that entry point; split_from = rows: none), with a merge of the
+ * split rows; d_work (16-byte aligned, >= uf_attn_split_rows_work_bytes, may
+ * be NULL when no row is split) is caller-owned scratch, overwritten.
+ * uf_attn_tail_plan picks split_from and n_split for a device with n_cu compute
+ * units: split_from = n_cu * floor(R / n_cu) and the n_split in 2..8 (in
+ * 2..min(64, n_cu / R) when R < n_cu) that makes the last round shortest,
+ * in row-times ceil((R - split_from) * n_split / n_cu) / n_split; it returns
+ * split_from = R and n_split = 1 (no split) when that saves under a fifth of a
+ * row-time, when R is a multiple of n_cu, or for 64-token tiles.  Results
+ * equal those of uf_sparse_causal_attn_fwd up to float rounding order.
+ * Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED (tile 64, except in the plan),
+ * UF_ERR_EMPTY, UF_ERR_HIP. */
+int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_t* n_split);
+int uf_attn_split_rows_work_bytes(const uf_kv* kv, int32_t split_from, int32_t n_split, size_t* bytes);
+int uf_sparse_causal_attn_fwd_split_rows(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
+                                         void* d_o, float* d_lse, int32_t split_from, int32_t n_split,
+                                         void* d_work, size_t work_bytes, void* stream);
+
 /* Backward of uf_sparse_causal_attn_fwd (the student's training side of
  * Sec. 2.3.1: gradients through the same Eq. 4 mask).  With p = exp(scale*q.k
  * - LSE) over the kept keys of each row, delta = <dO, O> per row and

@@ -41,6 +41,9 @@ from ._lib import (
     uf_sparse_causal_attn_fwd,
     uf_sparse_causal_attn_fwd_split,
     uf_attn_bwd_work_bytes,
+    uf_attn_split_rows_work_bytes,
+    uf_attn_tail_plan,
+    uf_sparse_causal_attn_fwd_split_rows,
     uf_sparse_causal_attn_bwd,
     uf_sparse_causal_attn_bwd_noalloc,
     uf_status_string,
@@ -54,6 +57,7 @@ __all__ = [
     "uf_topk_budget", "uf_topk_rule", "uf_kv_append",
     "uf_kv_create", "uf_kv_desc", "uf_kv_destroy", "uf_kv_evict", "uf_block_geom", "uf_block_geom_tokens", "uf_block_permute", "uf_kv_set_block_geom", "uf_kv_replace_newest", "uf_kv_get_info", "uf_kv_logical",
     "uf_kv_pool_bytes", "uf_last_error", "uf_sparse_causal_attn_fwd", "uf_sparse_causal_attn_fwd_split", "uf_attn_split_work_bytes",
-    "uf_attn_bwd_work_bytes", "uf_sparse_causal_attn_bwd", "uf_sparse_causal_attn_bwd_noalloc", "uf_status_string",
+    "uf_attn_bwd_work_bytes", "uf_attn_split_rows_work_bytes", "uf_attn_tail_plan",
+    "uf_sparse_causal_attn_fwd_split_rows", "uf_sparse_causal_attn_bwd", "uf_sparse_causal_attn_bwd_noalloc", "uf_status_string",
     "uf_tile_lists_bytes", "uf_tile_lists_layout", "KVWindow",
 ]

@@ -90,6 +90,12 @@ _SIGNATURES = {
     "uf_attn_split_work_bytes": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]),
     "uf_sparse_causal_attn_fwd_split": (ctypes.c_int, [_P, _P, _P, ctypes.c_float, _P, _P, ctypes.c_int32, _P,
                                                        ctypes.c_size_t, _P]),
+    "uf_attn_tail_plan": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                         ctypes.POINTER(ctypes.c_int32)]),
+    "uf_attn_split_rows_work_bytes": (ctypes.c_int, [_P, ctypes.c_int32, ctypes.c_int32,
+                                                     ctypes.POINTER(ctypes.c_size_t)]),
+    "uf_sparse_causal_attn_fwd_split_rows": (ctypes.c_int, [_P, _P, _P, ctypes.c_float, _P, _P, ctypes.c_int32,
+                                                            ctypes.c_int32, _P, ctypes.c_size_t, _P]),
     "uf_attn_bwd_work_bytes": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_size_t)]),
     "uf_sparse_causal_attn_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, ctypes.c_float, _P, _P, _P, _P,
                                                  ctypes.c_size_t, _P]),
@@ -256,6 +262,27 @@ def uf_sparse_causal_attn_fwd_split(handle, q, lists, scale: float, o, lse, n_sp
     s = None if q is None else _stream_ptr(stream)
     _check(load().uf_sparse_causal_attn_fwd_split(handle, _ptr(q), _ptr(lists), ctypes.c_float(scale), _ptr(o),
                                                   _ptr(lse), n_split, _ptr(work), n, s))
+
+
+def uf_attn_tail_plan(handle, n_cu: int):
+    """(split_from, n_split) that balances the last round of rows over n_cu compute units."""
+    f, s = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(load().uf_attn_tail_plan(handle, n_cu, ctypes.byref(f), ctypes.byref(s)))
+    return f.value, s.value
+
+
+def uf_attn_split_rows_work_bytes(handle, split_from: int, n_split: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().uf_attn_split_rows_work_bytes(handle, split_from, n_split, ctypes.byref(out)))
+    return out.value
+
+
+def uf_sparse_causal_attn_fwd_split_rows(handle, q, lists, scale: float, o, lse, split_from: int, n_split: int,
+                                         work, work_bytes: int = None, stream=None) -> None:
+    n = work_bytes if work_bytes is not None else (0 if work is None else work.numel() * work.element_size())
+    s = None if q is None else _stream_ptr(stream)
+    _check(load().uf_sparse_causal_attn_fwd_split_rows(handle, _ptr(q), _ptr(lists), ctypes.c_float(scale), _ptr(o),
+                                                       _ptr(lse), split_from, n_split, _ptr(work), n, s))
 
 
 def uf_attn_bwd_work_bytes(handle) -> int:

@@ -284,8 +284,9 @@ __device__ __forceinline__ void tri_second(TriState& st, float c2, const HalfCop
   st.l += rs1;
 }
 
-// SPLIT: workgroup (row, s) of a split-KV launch takes list entries
-// [s*count/split, (s+1)*count/split) of its row and writes its unnormalised
+// SPLIT: the first a.split_from workgroups run rows 0 .. split_from-1 whole;
+// each later row r is cut into a.split slices, and workgroup (r, s) takes list
+// entries [s*count/split, (s+1)*count/split) of it and writes its unnormalised
 // partial (O relative to its offset m, and l) to a.work; a merge combines them.
 // UNITS (windows with block geometry, whose tiles often hold 64 tokens or
 // fewer): the workgroup first lists its row's units that hold a valid key
@@ -296,8 +297,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   __shared__ uint4 sbuf[kBuffers][kHalf / 16];
   __shared__ uint32_t sunit[UNITS ? kUnitCap + 1 : 1];   // (j << 1) | key half; the count last
 
-  const int row = SPLIT ? int(blockIdx.x) / a.split : int(blockIdx.x);
-  const int part = SPLIT ? int(blockIdx.x) - row * a.split : 0;
+  int row = int(blockIdx.x), part = 0;
+  bool partial = false;               // this workgroup writes a split-KV partial
+  if (SPLIT && row >= a.split_from) {
+    const int k = row - a.split_from;
+    row = a.split_from + k / a.split;
+    part = k - (row - a.split_from) * a.split;
+    partial = true;
+  }
   const int qt = row % a.NT;
   const int bh = row / a.NT;
   const int h = bh % a.H;
@@ -340,8 +347,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   const uint8_t* head_pages = uniform_ptr(a.pool + (size_t(b) * a.H + h) * a.NT * pbytes);
   const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
   const int total = ((const const_i32*)a.counts)[row];
-  const int first = SPLIT ? int(int64_t(part) * total / a.split) : 0;
-  const int count = SPLIT ? int(int64_t(part + 1) * total / a.split) - first : total;
+  const int nsplit = partial ? a.split : 1;
+  const int first = partial ? int(int64_t(part) * total / nsplit) : 0;
+  const int count = partial ? int(int64_t(part + 1) * total / nsplit) - first : total;
   const float c2 = a.scale_log2;
   const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap + first;
   int U = 2 * count;                  // units
@@ -551,9 +559,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
       return st.o[mb][e] * fa + xo[((w1 * 4 + mb) * 16 + e) * 64 + lane] * fb +
              xo[((w2 * 4 + mb) * 16 + e) * 64 + lane] * fc;
     };
-    if (SPLIT) {
+    if (SPLIT && partial) {
       if (qvalid) {
-        const size_t wrow = size_t(row) * a.split + part;
+        const size_t wrow = size_t(row - a.split_from) * a.split + part;
         float* op = a.work + (wrow * kT + qw * 32 + ln) * kD;
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
@@ -568,7 +576,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
             *reinterpret_cast<float4*>(op + d0) = v;
           }
         if (hl == 0) {
-          float2* ml = reinterpret_cast<float2*>(a.work + size_t(a.B) * a.H * a.NT * a.split * kT * kD);
+          const size_t wrows = (size_t(a.B) * a.H * a.NT - a.split_from) * a.split;
+          float2* ml = reinterpret_cast<float2*>(a.work + wrows * kT * kD);
           ml[wrow * kT + qw * 32 + ln] = make_float2(mm, l);
         }
       }
@@ -596,7 +605,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
 // Split-KV merge: one workgroup per row; lane (query, half) combines the
 // row's partials for 64 dims: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
 __global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
-  const int row = blockIdx.x;
+  const int row = a.split_from + int(blockIdx.x);
   const int qt = row % a.NT;
   const int bh = row / a.NT;
   const int h = bh % a.H;
@@ -605,10 +614,11 @@ __global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
   const int half = threadIdx.x & 1;
   const int qrow = qt * kT + ql;
   if (qrow >= a.L) return;
-  const float2* ml = reinterpret_cast<const float2*>(a.work + size_t(a.B) * a.H * a.NT * a.split * kT * kD);
+  const size_t wrows = (size_t(a.B) * a.H * a.NT - a.split_from) * a.split;
+  const float2* ml = reinterpret_cast<const float2*>(a.work + wrows * kT * kD);
   float mm = -INFINITY;
   for (int s = 0; s < a.split; ++s) {
-    const float2 v = ml[(size_t(row) * a.split + s) * kT + ql];
+    const float2 v = ml[(size_t(row - a.split_from) * a.split + s) * kT + ql];
     if (v.y > 0.f) mm = fmaxf(mm, v.x);
   }
   float acc[64];
@@ -616,7 +626,7 @@ __global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
   for (int d = 0; d < 64; ++d) acc[d] = 0.f;
   float l = 0.f;
   for (int s = 0; s < a.split; ++s) {
-    const size_t wrow = size_t(row) * a.split + s;
+    const size_t wrow = size_t(row - a.split_from) * a.split + s;
     const float2 v = ml[wrow * kT + ql];
     if (!(v.y > 0.f)) continue;   // empty slice
     const float w = __builtin_amdgcn_exp2f(v.x - mm);
@@ -661,7 +671,8 @@ hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream) {
 }
 
 hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream) {
-  const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT) * unsigned(a.split);
+  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
+  const unsigned blocks = unsigned(a.split_from) + (rows - unsigned(a.split_from)) * unsigned(a.split);
   if (use_units(a))
     attn_fwd_tri_kernel<true, true><<<blocks, kThreads, 0, stream>>>(a);
   else
@@ -672,7 +683,8 @@ hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream)
 }
 
 hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream) {
-  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
+  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT) - unsigned(a.split_from);
+  if (rows == 0) return hipSuccess;
   attn_split_merge_kernel<<<rows, 256, 0, stream>>>(a);
   return hipGetLastError();
 }

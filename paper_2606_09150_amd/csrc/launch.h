@@ -98,8 +98,10 @@ struct AttnArgs {
   uint64_t nt_div;        // (2^64 - 1) / NT: j / NT == ((j + 1) * nt_div) >> 64 for 0 <= j < 2^31
   float scale;            // softmax scale
   float scale_log2;       // scale * log2(e)
-  int32_t split;          // list slices per row (split-KV), 1 = whole rows
-  float* work;            // split-KV partials: O [rows*split][T][D], then (m, l) [rows*split][T]
+  int32_t split;          // list slices per split row (split-KV), 1 = whole rows
+  int32_t split_from;     // split-KV: rows before this one run whole (0: every row is split)
+  float* work;            // split-KV partials of the split rows R = rows - split_from:
+                          // O [R*split][T][D], then (m, l) [R*split][T]
   int32_t slot_of[UF_MAX_CHUNKS];  // slot of each logical position
   TileValid tv;
 };
@@ -114,7 +116,7 @@ hipError_t launch_block_permute(const PermuteArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream);
-// combines the split-KV partials in a.work into O and LSE
+// combines the split-KV partials in a.work into O and LSE (rows split_from ..)
 hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream);
 
 inline hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {

@@ -420,6 +420,7 @@ int attn_args(const uf_kv* kv, const void* d_q, const void* d_lists, float scale
   a.scale = scale;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.split = 1;
+  a.split_from = 0;
   a.work = nullptr;
   a.tv = kv->tile_valid(0);
   for (size_t p = 0; p < kv->live.size(); ++p) a.slot_of[p] = kv->live[p].slot;
@@ -427,8 +428,9 @@ int attn_args(const uf_kv* kv, const void* d_q, const void* d_lists, float scale
   return UF_OK;
 }
 
-size_t split_work_bytes(const uf_kv* kv, int32_t n_split) {
-  const size_t rows = size_t(kv->layout().rows);
+// Partials of the rows split_from .. rows-1, n_split slices each.
+size_t split_work_bytes(const uf_kv* kv, int32_t n_split, int32_t split_from = 0) {
+  const size_t rows = size_t(kv->layout().rows) - size_t(split_from);
   return rows * size_t(n_split) * size_t(kv->d.tile) * (size_t(kv->d.head_dim) + 2) * 4;
 }
 
@@ -465,6 +467,68 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
   if (work_bytes < split_work_bytes(kv, n_split))
     return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, split_work_bytes(kv, n_split));
   a.split = n_split;
+  a.work = static_cast<float*>(d_work);
+  hipError_t e = uf::launch_attn_fwd_t128_tri_split(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_t* n_split) {
+  if (kv == nullptr || split_from == nullptr || n_split == nullptr) return fail(UF_ERR_ARG, "null argument");
+  if (n_cu < 1) return fail(UF_ERR_ARG, "n_cu must be >= 1");
+  const int64_t R = kv->layout().rows, C = n_cu;
+  *split_from = int32_t(R);
+  *n_split = 1;
+  if (kv->d.tile != 128) return ok();          // split-KV exists for 128-token tiles only
+  // time in row-times with one workgroup per CU and rounds of C workgroups:
+  // whole rows take ceil(R / C); rows F.. cut into S slices take
+  // F / C + ceil((R - F) * S / C) / S with F = C * floor(R / C)
+  const int64_t q = R / C, r = R % C;
+  if (r == 0) return ok();
+  const double whole = double(q + 1);
+  const int64_t s_max = q == 0 ? std::min<int64_t>(UF_MAX_SPLIT, std::max<int64_t>(2, C / R)) : 8;
+  double best = whole;
+  int32_t best_s = 1;
+  for (int64_t S = 2; S <= s_max; ++S) {
+    const double cost = double(q) + double((r * S + C - 1) / C) / double(S);
+    if (cost < best - 1e-9) {
+      best = cost;
+      best_s = int32_t(S);
+    }
+  }
+  if (best > whole - 0.2) return ok();        // under a fifth of a row-time saved: not worth the merge
+  *split_from = int32_t(q * C);
+  *n_split = best_s;
+  return ok();
+}
+
+int uf_attn_split_rows_work_bytes(const uf_kv* kv, int32_t split_from, int32_t n_split, size_t* bytes) {
+  if (kv == nullptr || bytes == nullptr) return fail(UF_ERR_ARG, "null argument");
+  if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
+  if (split_from < 0 || split_from > kv->layout().rows)
+    return fail(UF_ERR_ARG, "split_from must be in [0, %d]", kv->layout().rows);
+  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
+  *bytes = split_work_bytes(kv, n_split, split_from);
+  return ok();
+}
+
+int uf_sparse_causal_attn_fwd_split_rows(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
+                                         void* d_o, float* d_lse, int32_t split_from, int32_t n_split,
+                                         void* d_work, size_t work_bytes, void* stream) {
+  if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
+  if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
+  if (split_from < 0 || split_from > kv->layout().rows)
+    return fail(UF_ERR_ARG, "split_from must be in [0, %d]", kv->layout().rows);
+  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
+  uf::AttnArgs a{};
+  if (int s = attn_args(kv, d_q, d_lists, scale, d_o, d_lse, &a)) return s;
+  if (kv->dry()) return ok();
+  const size_t need = split_work_bytes(kv, n_split, split_from);
+  if (need > 0 && (d_work == nullptr || !aligned(d_work, 16)))
+    return fail(UF_ERR_ARG, "work must be non-null and 16-byte aligned");
+  if (work_bytes < need) return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, need);
+  a.split = n_split;
+  a.split_from = split_from;
   a.work = static_cast<float*>(d_work);
   hipError_t e = uf::launch_attn_fwd_t128_tri_split(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));

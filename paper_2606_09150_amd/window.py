@@ -125,7 +125,9 @@ class KVWindow:
         """O [B,L,H,D] bf16 (and LSE [B,H,L] fp32 when ``lse``) for the current chunk.
 
         ``split`` > 0 selects split-KV attention with that many list slices per
-        row; ``work`` is its scratch buffer (allocated here when None)."""
+        row; ``split="tail"`` splits only the rows of the last, partly filled
+        round of one workgroup per compute unit (uf_attn_tail_plan); ``work``
+        is the scratch buffer of either (allocated here when None)."""
         _check_chunk(q, "q", self.B, self.L, self.H, self.D)
         if scale is None:
             scale = 1.0 / math.sqrt(self.D)
@@ -143,7 +145,15 @@ class KVWindow:
         buf = self.lists if lists is None else lists
         if buf.numel() < self.layout.total_bytes:
             raise ValueError("list buffer too small")
-        if split:
+        if split == "tail":
+            n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
+            split_from, n_split = L.uf_attn_tail_plan(self.handle, n_cu)
+            need = L.uf_attn_split_rows_work_bytes(self.handle, split_from, n_split)
+            if work is None and need > 0:
+                work = torch.empty(need, dtype=torch.uint8, device=q.device)
+            L.uf_sparse_causal_attn_fwd_split_rows(self.handle, q, buf, scale, out, lse_t, split_from, n_split, work,
+                                                   None, stream)
+        elif split:
             need = L.uf_attn_split_work_bytes(self.handle, int(split))
             if work is None:
                 work = torch.empty(need, dtype=torch.uint8, device=q.device)

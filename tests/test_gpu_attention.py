@@ -389,3 +389,58 @@ def test_split_kv_480p_full():
     lerr = float(np.abs(f64(lse) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL and lerr <= lse_tol(128)
+
+
+def test_split_rows_parity_and_plan():
+    """Split-KV of the rows from split_from on only (the tail of the last
+    round): a small window with a mid split point against the oracle and the
+    unsplit kernel, then the 480p window with the plan for its 444 rows on 256
+    CUs (rows 256.. cut into 4 slices) in full against the oracle."""
+    P = require_gpu()
+    L = P._lib
+    log("attn split rows B=2 L=700 H=3 split_from=20 n_split=3")
+    case = Case(P, 2, 700, 3, 128, 5, True, seed=79)
+    for _ in range(6):
+        case.append()
+    rule = case.rule(0.5)
+    case.gpu_lists(rule)
+    q = case.query()
+    o1, l1 = case.attention(q)
+    o = torch.empty_like(q)
+    lse = torch.empty_like(l1)
+    work = torch.empty(L.uf_attn_split_rows_work_bytes(case.win.handle, 20, 3), dtype=torch.uint8, device="cuda")
+    L.uf_sparse_causal_attn_fwd_split_rows(case.win.handle, q, case.win.lists, 1 / math.sqrt(128), o, lse, 20, 3, work)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(o), O)
+    lerr = float(np.abs(f64(lse) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= lse_tol(128)
+    # rows before split_from run the unsplit code: bit-identical to the plain kernel
+    rows_whole = 20                  # rows (b*H + h)*NT + i with NT = 6
+    for r in range(rows_whole):
+        b, rem = divmod(r, 3 * 6)
+        h, i = divmod(rem, 6)
+        assert torch.equal(o[b, 128 * i:128 * (i + 1), h], o1[b, 128 * i:128 * (i + 1), h])
+
+    wl, case = _workload_case(P, "480p", "cuda")
+    for _ in range(wl.window_chunks):
+        case.append()
+    assert L.uf_attn_tail_plan(case.win.handle, 256) == (256, 4)
+    log("attn split rows 480p plan (256, 4)")
+    rule = case.rule(wl.p_prior)
+    case.gpu_lists(rule)
+    q = case.query()
+    o = torch.empty_like(q)
+    lse = torch.empty((1, wl.heads, wl.chunk_tokens), dtype=torch.float32, device="cuda")
+    work = torch.empty(L.uf_attn_split_rows_work_bytes(case.win.handle, 256, 4), dtype=torch.uint8, device="cuda")
+    L.uf_sparse_causal_attn_fwd_split_rows(case.win.handle, q, case.win.lists, 1 / math.sqrt(128), o, lse, 256, 4,
+                                           work)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, wl.tile, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(o), O)
+    lerr = float(np.abs(f64(lse) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= lse_tol(128)

@@ -34,7 +34,7 @@ def _declared():
 def test_library_exports_every_declared_symbol(P):
     from paper_2606_09150_amd import _lib
     names = _declared()
-    assert len(names) == 24
+    assert len(names) == 27
     lib = ctypes.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -294,3 +294,42 @@ def test_backward_host_paths(P):
     big.append(None, None)
     assert status(na, big.handle, *nargs) == L.UF_ERR_CAPACITY
     assert "1008 rows" in L.uf_last_error()
+
+
+def test_tail_plan_and_split_rows_host_paths(P):
+    L = P._lib
+    E = P.UfError
+
+    def status(fn, *a):
+        with pytest.raises(E) as ei:
+            fn(*a)
+        return ei.value.status
+
+    def plan(B, L_, H, n_cu, T=128):
+        w = _dry(P, max_chunks=2, L=L_, T=T, H=H, B=B)
+        return L.uf_attn_tail_plan(w.handle, n_cu)
+
+    # 480p: 444 rows on 256 CUs -> rows 256.. in 4 slices (1.75 row-times instead of 2)
+    assert plan(1, 4680, 12, 256) == (256, 4)
+    # 1K: 2,304 rows are nine whole rounds; 2K: 4,056 rows leave 216 in the last
+    # round, where no slice count saves a fifth of a row-time
+    assert plan(1, 24480, 12, 256) == (2304, 1)
+    assert plan(1, 43200, 12, 256) == (4056, 1)
+    # fewer rows than CUs: every row split, up to n_cu / rows slices
+    assert plan(1, 640, 1, 256) == (0, 51)
+    assert plan(1, 300, 2, 256) == (0, 42)
+    # 64-token tiles have no split-KV: no split
+    assert plan(1, 192, 2, 256, T=64) == (6, 1)
+    w = _dry(P, max_chunks=4, L=300, T=128, H=2)
+    rows = 2 * 3
+    assert L.uf_attn_split_rows_work_bytes(w.handle, 2, 3) == (rows - 2) * 3 * 128 * 130 * 4
+    assert L.uf_attn_split_rows_work_bytes(w.handle, rows, 3) == 0
+    assert status(L.uf_attn_split_rows_work_bytes, w.handle, rows + 1, 3) == L.UF_ERR_ARG
+    assert status(L.uf_attn_split_rows_work_bytes, w.handle, 0, 0) == L.UF_ERR_ARG
+    assert status(L.uf_attn_tail_plan, w.handle, 0) == L.UF_ERR_ARG
+    fn = L.uf_sparse_causal_attn_fwd_split_rows
+    assert status(fn, w.handle, None, None, 0.1, None, None, 0, 2, None, 0) == L.UF_ERR_EMPTY
+    w.append(None, None)
+    fn(w.handle, None, None, 0.1, None, None, 2, 3, None, 0)             # dry run
+    assert status(fn, w.handle, None, None, 0.1, None, None, -1, 3, None, 0) == L.UF_ERR_ARG
+    assert status(fn, w.handle, None, None, 0.1, None, None, 0, 65, None, 0) == L.UF_ERR_ARG
