@@ -107,11 +107,9 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     lse = torch.empty((B, H, L), dtype=torch.float32, device=dev)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
     work = None
+    n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
     if split == "tail":
-        n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
-        plan = P.uf_attn_tail_plan(win.handle, n_cu)
-        need = P.uf_attn_split_rows_work_bytes(win.handle, *plan)
-        work = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+        pass   # sized in the first (warm-up) step, once the window is full: the plan depends on its length
     elif split:
         work = torch.empty(P.uf_attn_split_work_bytes(win.handle, split), dtype=torch.uint8, device=dev)
     scale = 1.0 / math.sqrt(D)
@@ -127,6 +125,10 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
         e[1].record(stream)
         win.lists = lists[s]
         win.build_lists(wl.seed, wl.p_prior)
+        nonlocal work
+        if split == "tail" and work is None:
+            need = P.uf_attn_split_rows_work_bytes(win.handle, *P.uf_attn_tail_plan(win.handle, n_cu))
+            work = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
         e[2].record(stream)
         win.attention(src["q"], scale, out=out, lse=lse, split=split, work=work)
         e[3].record(stream)

@@ -297,9 +297,9 @@ int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_li
  * each slice leaves its unnormalised output, running offset and row sum in
  * d_work, and a merge combines them by the same log-sum-exp rescaling as the
  * online softmax.  d_work (16-byte aligned, >= uf_attn_split_work_bytes) is
- * caller-owned scratch, overwritten.  Needs 128-token tiles.  Results equal
- * those of uf_sparse_causal_attn_fwd up to float rounding order.  Errors:
- * UF_ERR_ARG, UF_ERR_UNSUPPORTED (tile 64), UF_ERR_EMPTY, UF_ERR_HIP. */
+ * caller-owned scratch, overwritten.  Both tile sizes.  Results equal those
+ * of uf_sparse_causal_attn_fwd up to float rounding order.  Errors:
+ * UF_ERR_ARG, UF_ERR_EMPTY, UF_ERR_HIP. */
 int uf_attn_split_work_bytes(const uf_kv* kv, int32_t n_split, size_t* bytes);
 int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,
                                     void* d_o, float* d_lse, int32_t n_split, void* d_work,
@@ -316,14 +316,16 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
  * split rows; d_work (16-byte aligned, >= uf_attn_split_rows_work_bytes, may
  * be NULL when no row is split) is caller-owned scratch, overwritten.
  * uf_attn_tail_plan picks split_from and n_split for a device with n_cu compute
- * units: split_from = n_cu * floor(R / n_cu) and the n_split in 2..8 (in
- * 2..min(64, n_cu / R) when R < n_cu) that makes the last round shortest,
- * in row-times ceil((R - split_from) * n_split / n_cu) / n_split; it returns
- * split_from = R and n_split = 1 (no split) when that saves under a fifth of a
- * row-time, when R is a multiple of n_cu, or for 64-token tiles.  Results
- * equal those of uf_sparse_causal_attn_fwd up to float rounding order.
- * Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED (tile 64, except in the plan),
- * UF_ERR_EMPTY, UF_ERR_HIP. */
+ * units, counting C = n_cu resident workgroups for 128-token tiles and 2 n_cu
+ * for 64-token tiles: split_from = C * floor(R / C) and the n_split in 2..8
+ * (in 2..min(64, C / R) when R < C), at most the window's key tiles, that
+ * makes the last round shortest, in row-times
+ * ceil((R - split_from) * n_split / C) / n_split; it returns split_from = R
+ * and n_split = 1 (no split) when R is a multiple of C or when the saving is
+ * under a fifth of a row-time or under 16 key tiles of one row's work (the
+ * window's key tiles times the saved row-time: short rows do not repay the
+ * merge launch).  Results equal those of uf_sparse_causal_attn_fwd
+ * up to float rounding order.  Errors: UF_ERR_ARG, UF_ERR_EMPTY, UF_ERR_HIP. */
 int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_t* n_split);
 int uf_attn_split_rows_work_bytes(const uf_kv* kv, int32_t split_from, int32_t n_split, size_t* bytes);
 int uf_sparse_causal_attn_fwd_split_rows(const uf_kv* kv, const void* d_q, const void* d_lists, float scale,

@@ -36,7 +36,11 @@ namespace {
 
 using namespace attn;
 
-template <int T>
+// SPLIT: as in the 128-token kernel, the first a.split_from workgroups run
+// rows 0 .. split_from-1 whole and every later row is cut into a.split slices
+// of its list; a slice writes its unnormalised O, its offset (base-2 units)
+// and its row sum to a.work for the merge.
+template <int T, bool SPLIT>
 __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
   constexpr int kWaves = T / 32;
   constexpr int kThreads = kWaves * 64;
@@ -49,7 +53,14 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
   __shared__ uint4 sK[T * kKC];
   __shared__ uint4 sV[kD * kVC];
 
-  const int row = blockIdx.x;
+  int row = int(blockIdx.x), part = 0;
+  bool partial = false;
+  if (SPLIT && row >= a.split_from) {
+    const int k = row - a.split_from;
+    row = a.split_from + k / a.split;
+    part = k - (row - a.split_from) * a.split;
+    partial = true;
+  }
   const int qt = row % a.NT;
   const int bh = row / a.NT;
   const int h = bh % a.H;
@@ -83,8 +94,10 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
   float m = -INFINITY;   // running (lazily raised) max of raw scores q.k
   float l = 0.f;         // running sum of bf16(exp2((s - m) * c2))
 
-  const int count = ((const const_i32*)a.counts)[row];
-  const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap;
+  const int total = ((const const_i32*)a.counts)[row];
+  const int first = partial ? int(int64_t(part) * total / a.split) : 0;
+  const int count = partial ? int(int64_t(part + 1) * total / a.split) - first : total;
+  const const_i32* list = (const const_i32*)a.idx + size_t(row) * a.nk_cap + first;
   const size_t pbytes = page_bytes(T, kD);
   const uint8_t* head_pages = a.pool + (size_t(b) * a.H + h) * a.NT * pbytes;
   const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
@@ -246,6 +259,27 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
     n = nn;
   }
 
+  if (SPLIT && partial) {
+    // partial: O relative to the offset m*c2 (base 2) and the row sum l
+    if (qvalid) {
+      const size_t wrow = size_t(row - a.split_from) * a.split + part;
+      float* op = a.work + (wrow * T + wave * 32 + ln) * kD;
+#pragma unroll
+      for (int mb = 0; mb < kD / 32; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d0 = mb * 32 + 8 * i + 4 * g;
+          *reinterpret_cast<float4*>(op + d0) = make_float4(o[mb][4 * i], o[mb][4 * i + 1], o[mb][4 * i + 2],
+                                                            o[mb][4 * i + 3]);
+        }
+      if (g == 0) {
+        const size_t wrows = (size_t(a.B) * a.H * a.NT - a.split_from) * a.split;
+        float2* ml = reinterpret_cast<float2*>(a.work + wrows * T * kD);
+        ml[wrow * T + wave * 32 + ln] = make_float2(m == -INFINITY ? -INFINITY : m * c2, l);
+      }
+    }
+    return;
+  }
   if (qvalid) {
     const float inv = (l > 0.f) ? 1.f / l : 0.f;
     uint16_t* op = a.o + ((size_t(b) * a.L + qrow) * a.H + h) * kD;
@@ -268,8 +302,17 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
 
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream) {
   const unsigned blocks = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
-  attn_fwd_kernel<64><<<blocks, 128, 0, stream>>>(a);
+  attn_fwd_kernel<64, false><<<blocks, 128, 0, stream>>>(a);
   return hipGetLastError();
+}
+
+hipError_t launch_attn_fwd_t64_split(const AttnArgs& a, hipStream_t stream) {
+  const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
+  const unsigned blocks = unsigned(a.split_from) + (rows - unsigned(a.split_from)) * unsigned(a.split);
+  attn_fwd_kernel<64, true><<<blocks, 128, 0, stream>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_attn_split_merge(a, stream);
 }
 
 }  // namespace uf

@@ -602,9 +602,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   }
 }
 
-// Split-KV merge: one workgroup per row; lane (query, half) combines the
+// Split-KV merge (tiles of TT tokens): one workgroup per split row; lane (query, half) combines the
 // row's partials for 64 dims: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
-__global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
+template <int TT>
+__global__ __launch_bounds__(2 * TT) void attn_split_merge_kernel(AttnArgs a) {
   const int row = a.split_from + int(blockIdx.x);
   const int qt = row % a.NT;
   const int bh = row / a.NT;
@@ -612,13 +613,13 @@ __global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
   const int b = bh / a.H;
   const int ql = threadIdx.x >> 1;
   const int half = threadIdx.x & 1;
-  const int qrow = qt * kT + ql;
+  const int qrow = qt * TT + ql;
   if (qrow >= a.L) return;
   const size_t wrows = (size_t(a.B) * a.H * a.NT - a.split_from) * a.split;
-  const float2* ml = reinterpret_cast<const float2*>(a.work + wrows * kT * kD);
+  const float2* ml = reinterpret_cast<const float2*>(a.work + wrows * TT * kD);
   float mm = -INFINITY;
   for (int s = 0; s < a.split; ++s) {
-    const float2 v = ml[(size_t(row - a.split_from) * a.split + s) * kT + ql];
+    const float2 v = ml[(size_t(row - a.split_from) * a.split + s) * TT + ql];
     if (v.y > 0.f) mm = fmaxf(mm, v.x);
   }
   float acc[64];
@@ -627,11 +628,11 @@ __global__ __launch_bounds__(256) void attn_split_merge_kernel(AttnArgs a) {
   float l = 0.f;
   for (int s = 0; s < a.split; ++s) {
     const size_t wrow = size_t(row - a.split_from) * a.split + s;
-    const float2 v = ml[wrow * kT + ql];
+    const float2 v = ml[wrow * TT + ql];
     if (!(v.y > 0.f)) continue;   // empty slice
     const float w = __builtin_amdgcn_exp2f(v.x - mm);
     l += v.y * w;
-    const float4* op = reinterpret_cast<const float4*>(a.work + (wrow * kT + ql) * kD + 64 * half);
+    const float4* op = reinterpret_cast<const float4*>(a.work + (wrow * TT + ql) * kD + 64 * half);
 #pragma unroll
     for (int c = 0; c < 16; ++c) {
       const float4 o = op[c];
@@ -685,7 +686,10 @@ hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream)
 hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream) {
   const unsigned rows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT) - unsigned(a.split_from);
   if (rows == 0) return hipSuccess;
-  attn_split_merge_kernel<<<rows, 256, 0, stream>>>(a);
+  if (a.T == 128)
+    attn_split_merge_kernel<128><<<rows, 256, 0, stream>>>(a);
+  else
+    attn_split_merge_kernel<64><<<rows, 128, 0, stream>>>(a);
   return hipGetLastError();
 }
 

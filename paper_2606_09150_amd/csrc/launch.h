@@ -116,11 +116,16 @@ hipError_t launch_block_permute(const PermuteArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t64(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_tri(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_attn_fwd_t128_tri_split(const AttnArgs& a, hipStream_t stream);
+hipError_t launch_attn_fwd_t64_split(const AttnArgs& a, hipStream_t stream);
 // combines the split-KV partials in a.work into O and LSE (rows split_from ..)
 hipError_t launch_attn_split_merge(const AttnArgs& a, hipStream_t stream);
 
 inline hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t stream) {
   return a.T == 128 ? launch_attn_fwd_t128_tri(a, stream) : launch_attn_fwd_t64(a, stream);
+}
+// split-KV launch (a.split, a.split_from, a.work set) and its merge
+inline hipError_t launch_attn_fwd_split(const AttnArgs& a, hipStream_t stream) {
+  return a.T == 128 ? launch_attn_fwd_t128_tri_split(a, stream) : launch_attn_fwd_t64_split(a, stream);
 }
 
 }  // namespace uf

@@ -449,7 +449,6 @@ int uf_sparse_causal_attn_fwd(const uf_kv* kv, const void* d_q, const void* d_li
 int uf_attn_split_work_bytes(const uf_kv* kv, int32_t n_split, size_t* bytes) {
   if (kv == nullptr || bytes == nullptr) return fail(UF_ERR_ARG, "null argument");
   if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
-  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
   *bytes = split_work_bytes(kv, n_split);
   return ok();
 }
@@ -459,7 +458,6 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
                                     void* stream) {
   if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
   if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
-  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
   uf::AttnArgs a{};
   if (int s = attn_args(kv, d_q, d_lists, scale, d_o, d_lse, &a)) return s;
   if (kv->dry()) return ok();
@@ -468,7 +466,7 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
     return fail(UF_ERR_ARG, "work has %zu bytes, needs %zu", work_bytes, split_work_bytes(kv, n_split));
   a.split = n_split;
   a.work = static_cast<float*>(d_work);
-  hipError_t e = uf::launch_attn_fwd_t128_tri_split(a, static_cast<hipStream_t>(stream));
+  hipError_t e = uf::launch_attn_fwd_split(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));
   return ok();
 }
@@ -476,17 +474,19 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
 int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_t* n_split) {
   if (kv == nullptr || split_from == nullptr || n_split == nullptr) return fail(UF_ERR_ARG, "null argument");
   if (n_cu < 1) return fail(UF_ERR_ARG, "n_cu must be >= 1");
-  const int64_t R = kv->layout().rows, C = n_cu;
+  // workgroups resident at once: one per CU with 128-token tiles, two with 64
+  const int64_t R = kv->layout().rows, C = int64_t(n_cu) * (kv->d.tile == 128 ? 1 : 2);
   *split_from = int32_t(R);
   *n_split = 1;
-  if (kv->d.tile != 128) return ok();          // split-KV exists for 128-token tiles only
-  // time in row-times with one workgroup per CU and rounds of C workgroups:
-  // whole rows take ceil(R / C); rows F.. cut into S slices take
+  // time in row-times with rounds of C workgroups: whole rows take
+  // ceil(R / C); rows F.. cut into S slices take
   // F / C + ceil((R - F) * S / C) / S with F = C * floor(R / C)
   const int64_t q = R / C, r = R % C;
   if (r == 0) return ok();
   const double whole = double(q + 1);
-  const int64_t s_max = q == 0 ? std::min<int64_t>(UF_MAX_SPLIT, std::max<int64_t>(2, C / R)) : 8;
+  // no more slices than key tiles in the window, so that no slice is empty by construction
+  const int64_t nk = int64_t(kv->live.size()) * kv->nt;
+  const int64_t s_max = std::min<int64_t>(nk, q == 0 ? std::min<int64_t>(UF_MAX_SPLIT, std::max<int64_t>(2, C / R)) : 8);
   double best = whole;
   int32_t best_s = 1;
   for (int64_t S = 2; S <= s_max; ++S) {
@@ -496,7 +496,9 @@ int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_
       best_s = int32_t(S);
     }
   }
-  if (best > whole - 0.2) return ok();        // under a fifth of a row-time saved: not worth the merge
+  // not worth the merge launch and the slices' fixed costs: under a fifth of
+  // a row-time, or under 16 key tiles of one row's work, saved
+  if (best > whole - 0.2 || (whole - best) * double(nk) < 16.0) return ok();
   *split_from = int32_t(q * C);
   *n_split = best_s;
   return ok();
@@ -507,7 +509,6 @@ int uf_attn_split_rows_work_bytes(const uf_kv* kv, int32_t split_from, int32_t n
   if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
   if (split_from < 0 || split_from > kv->layout().rows)
     return fail(UF_ERR_ARG, "split_from must be in [0, %d]", kv->layout().rows);
-  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
   *bytes = split_work_bytes(kv, n_split, split_from);
   return ok();
 }
@@ -519,7 +520,6 @@ int uf_sparse_causal_attn_fwd_split_rows(const uf_kv* kv, const void* d_q, const
   if (n_split < 1 || n_split > UF_MAX_SPLIT) return fail(UF_ERR_ARG, "n_split must be in [1, %d]", UF_MAX_SPLIT);
   if (split_from < 0 || split_from > kv->layout().rows)
     return fail(UF_ERR_ARG, "split_from must be in [0, %d]", kv->layout().rows);
-  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "split-KV needs 128-token tiles");
   uf::AttnArgs a{};
   if (int s = attn_args(kv, d_q, d_lists, scale, d_o, d_lse, &a)) return s;
   if (kv->dry()) return ok();
@@ -530,7 +530,7 @@ int uf_sparse_causal_attn_fwd_split_rows(const uf_kv* kv, const void* d_q, const
   a.split = n_split;
   a.split_from = split_from;
   a.work = static_cast<float*>(d_work);
-  hipError_t e = uf::launch_attn_fwd_t128_tri_split(a, static_cast<hipStream_t>(stream));
+  hipError_t e = uf::launch_attn_fwd_split(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(UF_ERR_HIP, "attn_fwd split launch: %s", hipGetErrorString(e));
   return ok();
 }

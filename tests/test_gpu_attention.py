@@ -444,3 +444,54 @@ def test_split_rows_parity_and_plan():
     lerr = float(np.abs(f64(lse) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL and lerr <= lse_tol(128)
+
+
+@pytest.mark.parametrize("n_split", [2, 3, 5])
+def test_split_kv_parity_t64(n_split):
+    """Split-KV with 64-token tiles (ragged tail, evictions, a pinned chunk)
+    against the oracle and the unsplit 64-token kernel."""
+    P = require_gpu()
+    log(f"attn split t64 n_split={n_split}")
+    case = Case(P, 1, 130, 2, 64, 3, True, seed=80)
+    for _ in range(5):
+        case.append()
+    rule = case.rule(0.4)
+    case.gpu_lists(rule)
+    q = case.query()
+    o1, l1 = case.attention(q)
+    os_, ls_ = case.win.attention(q, split=n_split)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 64, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(os_), O)
+    lerr = float(np.abs(f64(ls_) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= lse_tol(64)
+    assert row_rel_err(case._host(os_), case._host(o1)) <= REL_TOL
+
+
+def test_tiny_workload_split_rows():
+    """The tiny workload (6 rows of 64-token tiles, too short for the plan to
+    split) with every row cut into one slice per key tile, in full against the
+    oracle."""
+    P = require_gpu()
+    L = P._lib
+    wl, case = _workload_case(P, "tiny", "cpu")
+    for _ in range(wl.window_chunks):
+        case.append()
+    assert L.uf_attn_tail_plan(case.win.handle, 256) == (6, 1)
+    log("attn tiny split rows (0, 6)")
+    rule = case.rule(wl.p_prior)
+    case.gpu_lists(rule)
+    q = case.query()
+    o = torch.empty_like(q)
+    lse = torch.empty((1, wl.heads, wl.chunk_tokens), dtype=torch.float32, device="cuda")
+    work = torch.empty(L.uf_attn_split_rows_work_bytes(case.win.handle, 0, 6), dtype=torch.uint8, device="cuda")
+    L.uf_sparse_causal_attn_fwd_split_rows(case.win.handle, q, case.win.lists, 1 / math.sqrt(128), o, lse, 0, 6, work)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, wl.tile, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(o), O)
+    lerr = float(np.abs(f64(lse) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= lse_tol(64)

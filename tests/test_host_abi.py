@@ -246,11 +246,11 @@ def test_split_kv_host_paths(P):
     w.append(None, None)
     L.uf_sparse_causal_attn_fwd_split(w.handle, None, None, 0.1, None, None, 2, None, 0)   # dry run
     assert status(L.uf_sparse_causal_attn_fwd_split, w.handle, None, None, 0.1, None, None, 0, None, 0) == L.UF_ERR_ARG
+    # 64-token tiles: partials of 64 rows per slice
     w64 = _dry(P, max_chunks=2, L=300, T=64)
     w64.append(None, None)
-    assert status(L.uf_attn_split_work_bytes, w64.handle, 2) == L.UF_ERR_UNSUPPORTED
-    assert status(L.uf_sparse_causal_attn_fwd_split, w64.handle, None, None, 0.1, None, None, 2, None, 0) == \
-        L.UF_ERR_UNSUPPORTED
+    assert L.uf_attn_split_work_bytes(w64.handle, 2) == (2 * 5) * 2 * 64 * 130 * 4
+    L.uf_sparse_causal_attn_fwd_split(w64.handle, None, None, 0.1, None, None, 2, None, 0)   # dry run
 
 
 def test_backward_host_paths(P):
@@ -305,21 +305,27 @@ def test_tail_plan_and_split_rows_host_paths(P):
             fn(*a)
         return ei.value.status
 
-    def plan(B, L_, H, n_cu, T=128):
-        w = _dry(P, max_chunks=2, L=L_, T=T, H=H, B=B)
+    def plan(B, L_, H, n_cu, T=128, chunks=1):
+        w = _dry(P, max_chunks=max(2, chunks), L=L_, T=T, H=H, B=B)
+        for _ in range(chunks):
+            w.append(None, None)
         return L.uf_attn_tail_plan(w.handle, n_cu)
 
     # 480p: 444 rows on 256 CUs -> rows 256.. in 4 slices (1.75 row-times instead of 2)
-    assert plan(1, 4680, 12, 256) == (256, 4)
+    assert plan(1, 4680, 12, 256, chunks=4) == (256, 4)
     # 1K: 2,304 rows are nine whole rounds; 2K: 4,056 rows leave 216 in the last
     # round, where no slice count saves a fifth of a row-time
-    assert plan(1, 24480, 12, 256) == (2304, 1)
-    assert plan(1, 43200, 12, 256) == (4056, 1)
-    # fewer rows than CUs: every row split, up to n_cu / rows slices
-    assert plan(1, 640, 1, 256) == (0, 51)
-    assert plan(1, 300, 2, 256) == (0, 42)
-    # 64-token tiles have no split-KV: no split
-    assert plan(1, 192, 2, 256, T=64) == (6, 1)
+    assert plan(1, 24480, 12, 256, chunks=5) == (2304, 1)
+    assert plan(1, 43200, 12, 256, chunks=4) == (4056, 1)
+    # fewer rows than CUs: every row split, at most into as many slices as the
+    # window has key tiles (160 here), when rows are long enough to repay it
+    w = _dry(P, max_chunks=32, L=640, T=128, H=1)
+    for _ in range(32):
+        w.append(None, None)
+    assert L.uf_attn_tail_plan(w.handle, 256) == (0, 51)
+    # short rows (5 or 6 key tiles) are not split
+    assert plan(1, 640, 1, 256) == (5, 1)
+    assert plan(1, 192, 2, 256, T=64, chunks=2) == (6, 1)
     w = _dry(P, max_chunks=4, L=300, T=128, H=2)
     rows = 2 * 3
     assert L.uf_attn_split_rows_work_bytes(w.handle, 2, 3) == (rows - 2) * 3 * 128 * 130 * 4
