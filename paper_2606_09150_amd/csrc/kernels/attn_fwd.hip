@@ -36,6 +36,20 @@ namespace {
 
 using namespace attn;
 
+// With one wave per SIMD nothing hides an operand read's LDS latency but the
+// wave's own MFMAs: keep kAhead reads in flight, then one read per MFMA.
+template <int kReads>
+__device__ inline void schedule_reads_ahead() {
+  constexpr int kAhead = 8;
+  __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+  for (int i = 0; i < kReads - kAhead; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+}
+
 // SPLIT: as in the 128-token kernel, the first a.split_from workgroups run
 // rows 0 .. split_from-1 whole and every later row is cut into a.split slices
 // of its list; a slice writes its unnormalised O, its offset (base-2 units)
@@ -177,6 +191,7 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[kb], 0, 0, 0);
       }
     }
+    schedule_reads_ahead<KB * kD / 16>();
     __builtin_amdgcn_s_setprio(0);
     // every wave has its K operands in registers: the K buffer can be refilled
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
@@ -252,6 +267,7 @@ __global__ __launch_bounds__(T * 2, 2) void attn_fwd_kernel(AttnArgs a) {
           const bf16x8 vf = as_bf16x8(sV[d * kVC + (cc ^ (d & (kVC - 1)))]);
           o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hh], o[mb], 0, 0, 0);
         }
+    schedule_reads_ahead<KB * 2 * kD / 32>();
     __builtin_amdgcn_s_setprio(0);
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     __builtin_amdgcn_s_barrier();
