@@ -316,8 +316,8 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
  * split rows; d_work (16-byte aligned, >= uf_attn_split_rows_work_bytes, may
  * be NULL when no row is split) is caller-owned scratch, overwritten.
  * uf_attn_tail_plan picks split_from and n_split for a device with n_cu compute
- * units, counting C = n_cu resident workgroups for 128-token tiles and 2 n_cu
- * for 64-token tiles: split_from = C * floor(R / C) and the n_split in 2..8
+ * units, counting C = n_cu resident workgroups (one per compute unit with either
+ * tile size): split_from = C * floor(R / C) and the n_split in 2..8
  * (in 2..min(64, C / R) when R < C), at most the window's key tiles, that
  * makes the last round shortest, in row-times
  * ceil((R - split_from) * n_split / C) / n_split; it returns split_from = R

@@ -474,8 +474,8 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
 int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_t* n_split) {
   if (kv == nullptr || split_from == nullptr || n_split == nullptr) return fail(UF_ERR_ARG, "null argument");
   if (n_cu < 1) return fail(UF_ERR_ARG, "n_cu must be >= 1");
-  // workgroups resident at once: one per CU with 128-token tiles, two with 64
-  const int64_t R = kv->layout().rows, C = int64_t(n_cu) * (kv->d.tile == 128 ? 1 : 2);
+  // workgroups resident at once: one per CU with either tile size
+  const int64_t R = kv->layout().rows, C = int64_t(n_cu);
   *split_from = int32_t(R);
   *n_split = 1;
   // time in row-times with rounds of C workgroups: whole rows take
