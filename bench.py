@@ -569,6 +569,8 @@ def main():
                     "append_us", "append_gbps", "lists_us", "kept_fraction")
             others[name] = {k: r[k] for k in keep}
             others[name]["roofline_frac"] = r["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
+            if name == "tiny" and not args.no_bwd:
+                others[name]["backward"] = run_backward(P, synth.WORKLOADS[name], st2, reps=20)
             del st2
             if name == "480p":
                 # the same workload with the rows of the last, partly filled round split

@@ -345,9 +345,9 @@ int uf_sparse_causal_attn_fwd_split_rows(const uf_kv* kv, const void* d_q, const
  * Outputs, fp32, 16-byte aligned, fully overwritten: d_dq [B, L, H, D];
  * d_dk, d_dv [n_live, B, L, H, D] in logical chunk order (position 0 first).
  * d_work (16-byte aligned, >= uf_attn_bwd_work_bytes) is caller-owned scratch,
- * overwritten.  Deterministic (no atomics).  Needs 128-token tiles and
- * head_dim 128.  Errors: UF_ERR_ARG, UF_ERR_UNSUPPORTED (tile 64),
- * UF_ERR_EMPTY, UF_ERR_HIP. */
+ * overwritten.  Deterministic (no atomics).  Both tile sizes (at most 2,048
+ * query tiles per chunk), head_dim 128.  Errors: UF_ERR_ARG,
+ * UF_ERR_UNSUPPORTED (more query tiles), UF_ERR_EMPTY, UF_ERR_HIP. */
 int uf_attn_bwd_work_bytes(const uf_kv* kv, size_t* bytes);
 int uf_sparse_causal_attn_bwd(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do,
                               const float* d_lse, const void* d_lists, float scale, float* d_dq,

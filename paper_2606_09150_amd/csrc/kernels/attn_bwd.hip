@@ -50,20 +50,23 @@ __device__ inline float bf16f(uint16_t x) { return __uint_as_float(uint32_t(x) <
 
 // ---------------------------------------------------------------- prep ----
 
+// T-token tiles; a record always has room for 128 rows and 128 per-query
+// values, of which the first T are used.
+template <int T>
 __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(BwdArgs a) {
   const int row = blockIdx.x;                  // (b*H + h)*NT + i
   const int i = row % a.NT;
   const int bh = row / a.NT;
   const int h = bh % a.H, b = bh / a.H;
-  const int nv = tile_valid(a.tv, i, a.NT, a.tail, kT);
+  const int nv = tile_valid(a.tv, i, a.NT, a.tail, T);
   uint8_t* rec = a.work + size_t(row) * kBwdQTile;
   uint4* qr = reinterpret_cast<uint4*>(rec);
   uint4* orow = reinterpret_cast<uint4*>(rec + kTile);
-  for (int c = threadIdx.x; c < kT * 16; c += kThreads) {
+  for (int c = threadIdx.x; c < T * 16; c += kThreads) {
     const int r = c >> 4, cc = c & 15;
     uint4 vq = make_uint4(0, 0, 0, 0), vo = vq;
     if (r < nv) {
-      const size_t off = ((size_t(b) * a.L + size_t(i) * kT + r) * a.H + h) * kD + cc * 8;
+      const size_t off = ((size_t(b) * a.L + size_t(i) * T + r) * a.H + h) * kD + cc * 8;
       vq = *reinterpret_cast<const uint4*>(a.q + off);
       vo = *reinterpret_cast<const uint4*>(a.dout + off);
     }
@@ -72,11 +75,11 @@ __global__ __launch_bounds__(kThreads) void bwd_prep_kernel(BwdArgs a) {
   }
   float* nlse = reinterpret_cast<float*>(rec + 2 * kTile);
   float* ndelta = nlse + kT;
-  if (threadIdx.x < kT) {
+  if (threadIdx.x < T) {
     const int q = threadIdx.x;
     float nl = -INFINITY, dl = 0.f;
     if (q < nv) {
-      const size_t tok = size_t(i) * kT + q;
+      const size_t tok = size_t(i) * T + q;
       nl = -a.lse[(size_t(b) * a.H + h) * a.L + tok] / a.scale;
       const uint16_t* op = a.o + ((size_t(b) * a.L + tok) * a.H + h) * kD;
       const uint16_t* gp = a.dout + ((size_t(b) * a.L + tok) * a.H + h) * kD;
@@ -201,9 +204,9 @@ __device__ inline bf16x8 row_op(const uint8_t* tile, const RowTable& U, int R, i
 
 // ---------------------------------------------------------------- dkdv ----
 
-// One workgroup per window key tile kj = ((pos*B + b)*H + h)*NT + t, eight
-// waves: wave w < 4 (group 0) and wave w + 4 (group 1) share keys
-// 32w + swap23(ln) (lane ln), so that the V operand read transposed from the
+// One workgroup per window key tile kj = ((pos*B + b)*H + h)*NT + t, T/16
+// waves (eight for 128-token tiles): wave w < T/32 (group 0) and wave
+// w + T/32 (group 1) share keys 32w + swap23(ln) (lane ln), so that the V operand read transposed from the
 // pool's V^T tile (whose columns hold the keys in swap23 order) lands in
 // natural lane order.  Per 32-query block, group 0 computes S = Q K^T and P,
 // hands P (bf16, already in the B-operand layout) to its partner through LDS
@@ -213,16 +216,31 @@ __device__ inline bf16x8 row_op(const uint8_t* tile, const RowTable& U, int R, i
 // dS = P dP' need no subtraction.  Both groups issue the same number of MFMAs
 // and one SIMD runs one wave of each.  The kept query tiles are gathered first
 // (mask bits); their Q and dO rows are double-buffered in LDS.
-constexpr int kDkdvThreads = 512;
-
 __device__ inline uint32_t copy_offset8(int wave, int lane) {
   const int r = 4 * wave + (lane >> 4);
   return uint32_t(r * 256 + swz_perm((lane & 15) ^ swz_f(r & 15)) * 16);
 }
-// eight waves: copy i of wave w fills LDS chunks [64*(8i + w), +64), rows 32i + 4w + lane/16
-__device__ inline void copy_tile8(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
+// A T-row tile of 256-byte rows with W = T/16 waves: copy i of wave w fills
+// LDS chunks [64*(W i + w), +64), rows 4(W i + w) + lane/16; the row's low
+// four bits do not depend on i.
+template <int W>
+__device__ inline void copy_tile_w(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dma16(src + i * 8192, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 8192u);
+  for (int i = 0; i < 4; ++i)
+    dma16(src + i * (W * 1024), voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * uint32_t(W * 1024));
+}
+// The V^T of a 64-token page ([128 dims][64 keys], 128-byte rows) into the
+// swizzled [128][128] tile layout, of which it fills the first 64 columns,
+// with four waves: copy i of wave w fills rows 16i + 4w + lane/16.  A lane
+// whose LDS position holds one of the unused columns 64..127 fetches a
+// duplicate of a used chunk of its row (in bounds, never read).
+__device__ inline uint32_t copy_offset_vt64(int wave, int lane) {
+  const int r = 4 * wave + (lane >> 4);
+  return uint32_t(r * 128 + (swz_perm((lane & 15) ^ swz_f(r)) & 7) * 16);
+}
+__device__ inline void copy_vt64_w4(const uint8_t* src, uint32_t lds_tile, uint32_t voff, int wave) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) dma16(src + i * 2048, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 4096u);
 }
 __device__ inline uint32_t copy_offset8_page(int wave, int lane) {
   const int r = 4 * wave + (lane >> 4);
@@ -233,8 +251,13 @@ __device__ inline void copy_tile8_page(const uint8_t* src, uint32_t lds_tile, ui
   for (int i = 0; i < 4; ++i) dma16(src + i * 4096, voff, lds_tile + uint32_t(wave) * 1024u + uint32_t(i) * 8192u);
 }
 
-__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
-  __shared__ uint4 sQ[2][kT * 16], sO[2][kT * 16];   // Q and dO rows, two query tiles (128 KB)
+template <int T>
+__global__ __launch_bounds__(4 * T, 1) void bwd_dkdv_kernel(BwdArgs a) {
+  constexpr int kKW = T / 32;                        // key blocks = waves of a group
+  constexpr int kQB = T / 32;                        // 32-query blocks of a query tile
+  // Q and dO rows, two query tiles (128 KB); the second dO buffer first holds
+  // the page's V^T (128 rows)
+  __shared__ uint4 sQ[2][kT * 16], sO[2][kT * 16];
   __shared__ uint4 sP[4 * 2 * 2 * 64];               // P operands: [wave pair][block of the half][kk][lane]
   __shared__ float sLD[2][2 * kT];                   // -LSE/scale, then -delta, per buffer
   __shared__ uint16_t sList[kBwdMaxQTiles];
@@ -248,10 +271,10 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   const int h = bh % a.H, b = bh / a.H;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 2, kw = wave & 3;
+  const int grp = wave / kKW, kw = wave % kKW;
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
   const uint32_t voff = copy_offset8(wave, lane);
-  const int kvalid = tile_valid(a.tv, t, a.NT, a.tail, kT);
+  const int kvalid = tile_valid(a.tv, t, a.NT, a.tail, T);
   const int key = kw * 32 + swap23(ln);         // this lane's key (result column)
   const bool key_ok = key < kvalid;
   const int j = pos * a.NT + t;                 // logical key tile
@@ -259,14 +282,19 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 
   // B operands of the wave's keys: group 0 K rows from the page, group 1 V
   // read transposed from the page's V^T staged in the second dO buffer
-  const uint8_t* page = a.pool + ((size_t(a.slot_of[pos]) * a.B * a.H + bh) * a.NT + t) * page_bytes(kT, kD);
+  const uint8_t* page = a.pool + ((size_t(a.slot_of[pos]) * a.B * a.H + bh) * a.NT + t) * page_bytes(T, kD);
   bf16x8 bop[8];
   if (grp == 0) {
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      bop[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + page_chunk(key, 2 * ks + hl)));
+    for (int ks = 0; ks < 8; ++ks) {
+      const uint32_t off = T == 128 ? page_chunk(key, 2 * ks + hl) : uint32_t(key * 256 + (2 * ks + hl) * 16);
+      bop[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(page + off));
+    }
   }
-  copy_tile8_page(page + kTile, lds_addr(&sO[1][0]), copy_offset8_page(wave, lane), wave);
+  if constexpr (T == 128)
+    copy_tile8_page(page + kTile, lds_addr(&sO[1][0]), copy_offset8_page(wave, lane), wave);
+  else
+    copy_vt64_w4(page + T * kD * 2, lds_addr(&sO[1][0]), copy_offset_vt64(wave, lane), wave);
 
   // kept query tiles, ascending
   if (wave == 0) {
@@ -301,8 +329,8 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
   auto record = [&](int n) { return qbase + size_t(__builtin_amdgcn_readfirstlane(int(sList[n]))) * kBwdQTile; };
   auto issue = [&](int n) {
     const uint8_t* rec = record(n);
-    copy_tile8(rec, lds_addr(&sQ[n & 1][0]), voff, wave);
-    copy_tile8(rec + kTile, lds_addr(&sO[n & 1][0]), voff, wave);
+    copy_tile_w<T / 16>(rec, lds_addr(&sQ[n & 1][0]), voff, wave);
+    copy_tile_w<T / 16>(rec + kTile, lds_addr(&sO[n & 1][0]), voff, wave);
     if (wave == 0) dma16(rec + 2 * kTile, uint32_t(lane) * 16u, lds_addr(&sLD[n & 1][0]));
   };
 
@@ -347,7 +375,7 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     f32x16 p;
 #pragma unroll
     for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(sv[r] * c2);
-    if (kvalid < kT) {                          // padding keys (lanes) weigh nothing
+    if (kvalid < T) {                           // padding keys (lanes) weigh nothing
 #pragma unroll
       for (int r = 0; r < 16; ++r) p[r] = key_ok ? p[r] : 0.f;
     }
@@ -371,12 +399,13 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     accumulate(lq, qb, op);
   };
 
-  // Per tile, five steps separated by meetings; P slot qb&1 carries block qb
-  // from group 0 (step qb) to group 1 (step qb+1):
-  //   step 0: group 0 S, P of block 0            | group 1 dP of block 0
-  //   step s: group 0 S, P of block s, dV of s-1 | group 1 dS, dK of s-1, dP of s
-  //   step 4: group 0 dV of block 3              | group 1 dS, dK of block 3
-  // so that in the three middle steps both waves of a SIMD have 16 MFMAs.
+  // Per tile, kQB + 1 steps (five for 128-token tiles) separated by
+  // meetings; P slot qb&1 carries block qb from group 0 (step qb) to group 1
+  // (step qb+1):
+  //   step 0:   group 0 S, P of block 0            | group 1 dP of block 0
+  //   step s:   group 0 S, P of block s, dV of s-1 | group 1 dS, dK of s-1, dP of s
+  //   step kQB: group 0 dV of the last block       | group 1 dS, dK of the last block
+  // so that in the middle steps both waves of a SIMD have 16 MFMAs.
   // The buffer of tile n is n&1; the loop runs two tiles per trip so that the
   // buffer, and with it every operand address, is a compile-time offset.
   // Each group runs its own copy of the tile loop (same meetings in the same
@@ -394,15 +423,15 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
     bf16x8 op[2][2];                            // group 0: P operands of the last two blocks
     f32x16 dpv[2];                              // group 1: dP - delta of the last two blocks
 #pragma unroll
-    for (int st = 0; st < 5; ++st) {
+    for (int st = 0; st <= kQB; ++st) {
       if constexpr (G == 0) {
-        if (st < 4) scores(lq, ld, st, op[st & 1]);
+        if (st < kQB) scores(lq, ld, st, op[st & 1]);
         if (st > 0) accumulate((const lds_u8*)lo, st - 1, op[(st - 1) & 1]);   // dV^T += dO^T P
       } else {
         if (st > 0) dk_block((const lds_u8*)lq, st - 1, dpv[(st - 1) & 1]);
-        if (st < 4) dpv[st & 1] = product(lo, ld + kT, st);
+        if (st < kQB) dpv[st & 1] = product(lo, ld + kT, st);
       }
-      if (st < 4) __syncthreads();              // P of block st written; block st-1 consumed
+      if (st < kQB) __syncthreads();            // P of block st written; block st-1 consumed
     }
   };
   auto run = [&](auto group) {
@@ -418,7 +447,7 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 
   // store: lane holds key `key`, dims mb*32 + 8*(r/4) + 4*hl + r%4; padding
   // rows inside the chunk (block order) get the zeros they accumulated
-  const size_t tok = size_t(t) * kT + key;
+  const size_t tok = size_t(t) * T + key;
   if (tok < size_t(a.L)) {
     float* dst = (grp ? a.dk : a.dv) + (((size_t(pos) * a.B + b) * a.L + tok) * a.H + h) * kD;
     const float f = grp ? a.scale : 1.0f;
@@ -438,8 +467,11 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(BwdArgs a) {
 // operand arrives when read transposed from the page's V^T; K rows are read
 // in the same order.  dS^T as a B operand then holds natural key order.
 // Entries naming a tile outside the window count no key.
-__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
-  __shared__ uint4 sK[kT * 16], sV[kD * 16];    // K rows and V^T of one page (64 KB)
+template <int T>
+__global__ __launch_bounds__(2 * T, 2) void bwd_dq_kernel(BwdArgs a) {
+  // K rows and V^T of one page in the swizzled 256-byte-row layout (64 KB;
+  // a 64-token page fills K's first 64 rows and V^T's first 64 columns)
+  __shared__ uint4 sK[kT * 16], sV[kD * 16];
 
   const int row = blockIdx.x;                  // (b*H + h)*NT + i
   const int i = row % a.NT;
@@ -448,7 +480,20 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, hl = lane >> 5, ln = lane & 31;
-  const uint32_t voff = copy_offset_page(wave, lane);
+  // copy offsets: 128-token pages with four waves, one offset for every copy;
+  // 64-token pages with two waves, copy i of wave w filling rows
+  // 8i + 4w + lane/16, whose low four bits depend on i % 2
+  uint32_t voff = 0, koff64[2] = {0, 0}, voff64[2] = {0, 0};
+  if constexpr (T == 128) {
+    voff = copy_offset_page(wave, lane);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int r = 4 * wave + (lane >> 4) + 8 * k;
+      koff64[k] = uint32_t(r * 256 + swz_perm((lane & 15) ^ swz_f(r)) * 16);
+      voff64[k] = uint32_t(r * 128 + (swz_perm((lane & 15) ^ swz_f(r)) & 7) * 16);
+    }
+  }
   const int q = wave * 32 + ln;                 // this lane's query (result column)
   const lds_u8* lk = (const lds_u8*)sK;
   const lds_u8* lv = (const lds_u8*)sV;
@@ -479,7 +524,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   const float c2 = a.scale_log2;
   const int N = ((const const_i32*)a.counts)[row];
   const const_i32* list = ((const const_i32*)a.idx) + size_t(row) * a.nk_cap;
-  const size_t pbytes = page_bytes(kT, kD);
+  const size_t pbytes = page_bytes(T, kD);
   const uint8_t* head_pages = a.pool + size_t(bh) * a.NT * pbytes;
   const size_t slot_stride = size_t(a.B) * a.H * a.NT * pbytes;
 
@@ -489,16 +534,26 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
     const uint8_t* page = head_pages + size_t(a.slot_of[0]) * slot_stride;
     if (unsigned(j) < unsigned(a.nk)) {
       const int pos = j / a.NT, t = j - pos * a.NT;
-      kvalid = tile_valid(a.tv, t, a.NT, a.tail, kT);
+      kvalid = tile_valid(a.tv, t, a.NT, a.tail, T);
       page = head_pages + size_t(a.slot_of[pos]) * slot_stride + size_t(t) * pbytes;
     }
     __syncthreads();                            // previous tile consumed
-    copy_tile_page(page, lds_addr(sK), voff, wave);
-    copy_tile_page(page + kTile, lds_addr(sV), voff, wave);
+    if constexpr (T == 128) {
+      copy_tile_page(page, lds_addr(sK), voff, wave);
+      copy_tile_page(page + kTile, lds_addr(sV), voff, wave);
+    } else {
+      // K: 64 rows of 256 bytes, 8 copies; V^T: 128 rows of 128 bytes, 16 copies
+      const uint32_t lk0 = lds_addr(sK) + uint32_t(wave) * 1024u, lv0 = lds_addr(sV) + uint32_t(wave) * 1024u;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) dma16(page + (c >> 1) * 4096, koff64[c & 1], lk0 + uint32_t(c) * 2048u);
+#pragma unroll
+      for (int c = 0; c < 16; ++c)
+        dma16(page + T * kD * 2 + (c >> 1) * 2048, voff64[c & 1], lv0 + uint32_t(c) * 2048u);
+    }
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < T / 32; ++kb) {
       // S^T = K Q^T and dP^T = V dO^T: A operands are K rows kb*32 + swap23(ln)
       // and V read transposed from V^T (tile row = dim, columns kb*32 ..);
       f32x16 sv, dpv;
@@ -510,7 +565,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
       }
       // keys past the tile's valid rows get -inf, so their weights vanish (a
       // rare case: the key indices are formed here, not held across the loop)
-      if (kvalid < kT) {
+      if (kvalid < T) {
         int h4 = 4 * hl;
         asm volatile("" : "+v"(h4));
 #pragma unroll
@@ -533,8 +588,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdArgs a) {
   }
 
   // padding rows inside the chunk accumulated zeros (their seed is -inf)
-  if (size_t(i) * kT + q < size_t(a.L)) {
-    const size_t base = ((size_t(b) * a.L + size_t(i) * kT + q) * a.H + h) * kD;
+  if (size_t(i) * T + q < size_t(a.L)) {
+    const size_t base = ((size_t(b) * a.L + size_t(i) * T + q) * a.H + h) * kD;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -599,16 +654,27 @@ hipError_t launch_attn_bwd_noalloc(BwdArgs a, hipStream_t stream) {
   return launch_attn_bwd(a, stream);
 }
 
-hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream) {
+namespace {
+
+template <int T>
+hipError_t launch_bwd_t(const BwdArgs& a, hipStream_t stream) {
   const unsigned qrows = unsigned(a.B) * unsigned(a.H) * unsigned(a.NT);
   const unsigned ktiles = unsigned(a.n_live) * qrows;
-  bwd_prep_kernel<<<qrows, kThreads, 0, stream>>>(a);
+  bwd_prep_kernel<T><<<qrows, kThreads, 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  bwd_dkdv_kernel<<<ktiles, kDkdvThreads, 0, stream>>>(a);
+  bwd_dkdv_kernel<T><<<ktiles, 4 * T, 0, stream>>>(a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  bwd_dq_kernel<<<qrows, kThreads, 0, stream>>>(a);
+  bwd_dq_kernel<T><<<qrows, 2 * T, 0, stream>>>(a);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd(const BwdArgs& a, hipStream_t stream) {
+  if (a.T == 128) return launch_bwd_t<128>(a, stream);
+  if (a.T == 64) return launch_bwd_t<64>(a, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace uf

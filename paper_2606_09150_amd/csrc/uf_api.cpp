@@ -544,7 +544,6 @@ size_t bwd_work_bytes(const uf_kv* kv) { return size_t(kv->layout().rows) * uf::
 
 int uf_attn_bwd_work_bytes(const uf_kv* kv, size_t* bytes) {
   if (kv == nullptr || bytes == nullptr) return fail(UF_ERR_ARG, "null argument");
-  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "the backward needs 128-token tiles");
   *bytes = bwd_work_bytes(kv);
   return ok();
 }
@@ -557,7 +556,6 @@ int bwd_args(const uf_kv* kv, const void* d_q, const void* d_o, const void* d_do
              const void* d_lists, float scale, float* d_dq, float* d_dk, float* d_dv, bool work, void* d_work,
              size_t work_bytes, uf::BwdArgs* out) {
   if (kv == nullptr) return fail(UF_ERR_ARG, "handle is null");
-  if (kv->d.tile != 128) return fail(UF_ERR_UNSUPPORTED, "the backward needs 128-token tiles");
   if (kv->nt > uf::kBwdMaxQTiles) return fail(UF_ERR_UNSUPPORTED, "the backward handles at most %d query tiles", uf::kBwdMaxQTiles);
   uf::AttnArgs f{};
   if (int s = attn_args(kv, d_q, d_lists, scale, const_cast<void*>(d_o), const_cast<float*>(d_lse), &f)) return s;

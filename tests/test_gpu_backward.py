@@ -94,14 +94,26 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("T", [128, 64])
 @pytest.mark.parametrize("B,L,H,mc,pin,n,p", SMALL)
-def test_small_backward_parity(B, L, H, mc, pin, n, p):
+def test_small_backward_parity(B, L, H, mc, pin, n, p, T):
     P = require_gpu()
-    log(f"bwd small B={B} L={L} H={H} max={mc} pin={pin} n={n} p={p}")
-    case = Case(P, B, L, H, 128, mc, pin, seed=2000 + L + H)
+    log(f"bwd small T={T} B={B} L={L} H={H} max={mc} pin={pin} n={n} p={p}")
+    case = Case(P, B, L, H, T, mc, pin, seed=2000 + L + H)
     for _ in range(n):
         case.append()
     _full_compare(case, case.rule(p))
+
+
+def test_backward_tiny_workload():
+    """The tiny window (64-token tiles, 2 heads, 384 keys, every tile kept) in full."""
+    P = require_gpu()
+    wl = synth.WORKLOADS["tiny"]
+    log("bwd workload=tiny")
+    case = Case(P, wl.batch, wl.chunk_tokens, wl.heads, wl.tile, wl.max_chunks, wl.pin_sink, wl.seed)
+    for _ in range(wl.window_chunks):
+        case.append()
+    _full_compare(case, case.rule(wl.p_prior))
 
 
 def test_backward_large_logits():
@@ -136,14 +148,15 @@ def test_backward_large_logits():
     assert max(worst["dq"], worst["dk"], worst["dv"], worst["dv_plain"]) <= GRAD_TOL, worst
 
 
-def test_backward_poisoned_padding_and_determinism():
+@pytest.mark.parametrize("T", [128, 64])
+def test_backward_poisoned_padding_and_determinism(T):
     """Padding keys (bf16 9984.0 in the pool) never count, bit for bit, and two
     runs give identical gradients (no atomics)."""
     P = require_gpu()
-    log("bwd poison pad + determinism")
+    log(f"bwd poison pad + determinism T={T}")
     outs = []
     for flags in (0, P._lib.UF_F_POISON_PAD):
-        case = Case(P, 1, 300, 2, 128, 3, True, seed=2102, flags=flags)
+        case = Case(P, 1, 300, 2, T, 3, True, seed=2102, flags=flags)
         for _ in range(3):
             case.append()
         outs.append(_run(case, case.rule(0.5))[4:])

@@ -178,7 +178,7 @@ def test_paper_geometry_1k_local_window():
     case.check_attention(q, bits, heads=[0, 3], blocks=[0, 14, 134, 269])
 
 
-G128 = oracle.BlockGeom(3, 10, 12, 2, 8, 8)     # 8 blocks of 128 (the backward needs 128-token tiles)
+G128 = oracle.BlockGeom(3, 10, 12, 2, 8, 8)     # 8 blocks of 128 tokens, edge blocks partial
 
 
 @pytest.mark.parametrize("r", [0, 1])
@@ -206,31 +206,32 @@ def test_blocked_128_attention_skips_empty_key_halves(r):
     assert float((l3[:, :, valid] - l1[:, :, valid]).abs().max()) <= lse_tol(128)
 
 
+@pytest.mark.parametrize("g", [G128, SMALL], ids=["blocks128", "blocks64"])
 @pytest.mark.parametrize("r", [0, 1])
-def test_blocked_backward(r):
+def test_blocked_backward(r, g):
     """dQ, dK, dV on block-ordered tokens (uf_sparse_causal_attn_bwd with block
     geometry) mapped back to raster order, against the oracle's raster-order
     gradients; padding rows are exactly zero.  Bar: per gradient row,
     max_d|diff| / max_d|ref| <= 1e-2, as for the raster backward."""
     P = require_gpu()
-    log(f"blocks backward r={r}")
-    case = BlockCase(P, G128, 2, 2, 4, True, seed=49)
+    log(f"blocks backward r={r} tile={g.tile}")
+    case = BlockCase(P, g, 2, 2, 4, True, seed=49)
     for _ in range(5):
         case.append()
     case.win.build_lists(case.seed, 0.5, local_r=r)
     bits = case.oracle_bernoulli(0.5, r)
     q, do = case.draw(99, "q"), case.draw(99, "do")
-    qb, dob = _permute(P, G128, q, 0), _permute(P, G128, do, 0)
+    qb, dob = _permute(P, g, q, 0), _permute(P, g, do, 0)
     o, lse = case.win.attention(qb)
     dq, dk, dv = case.win.attention_bwd(qb, o, lse, dob)
     torch.cuda.synchronize()
-    src = oracle.block_order(G128)
+    src = oracle.block_order(g)
     valid = src >= 0
     gq, gk, gv = dq.cpu().numpy(), dk.cpu().numpy(), dv.cpu().numpy()
     assert np.all(gq[:, ~valid] == 0) and np.all(gk[:, :, ~valid] == 0) and np.all(gv[:, :, ~valid] == 0)
-    rq = np.zeros((case.B, G128.tokens, case.H, 128))
+    rq = np.zeros((case.B, g.tokens, case.H, 128))
     rq[:, src[valid]] = gq[:, valid]
-    rk = np.zeros((gk.shape[0], case.B, G128.tokens, case.H, 128))
+    rk = np.zeros((gk.shape[0], case.B, g.tokens, case.H, 128))
     rv = np.zeros_like(rk)
     rk[:, :, src[valid]] = gk[:, :, valid]
     rv[:, :, src[valid]] = gv[:, :, valid]
@@ -240,7 +241,7 @@ def test_blocked_backward(r):
     for b in range(case.B):
         for h in range(case.H):
             wq, wk, wv = oracle.attention_in_raster_bwd([c.k[b, :, h] for c in chunks], [c.v[b, :, h] for c in chunks],
-                                                        qh[b, :, h], doh[b, :, h], G128, bits[b, h], 1 / math.sqrt(128))
+                                                        qh[b, :, h], doh[b, :, h], g, bits[b, h], 1 / math.sqrt(128))
             for got, want in ((rq[b, :, h], wq), (rk[:, b, :, h], np.stack(wk)), (rv[:, b, :, h], np.stack(wv))):
                 worst = max(worst, float(row_errors(got, want).max()))
     log(f"  per-row={worst:.3e}")

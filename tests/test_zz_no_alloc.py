@@ -3,9 +3,9 @@ ABI) against the allocating entry point, uf_sparse_causal_attn_bwd.
 
 Both run the same kernels on the same query-tile records, the first from the
 library's own device scratch and the second from the caller's workspace, so
-the gradients must agree bit for bit.  Two no-allocation calls run in a row,
-the second on a smaller window, so that it reads the scratch after the first
-call left its records there; the outputs start as NaN so that any element a
+the gradients must agree bit for bit.  Three no-allocation calls run in a
+row, each later one on a smaller window (the last with 64-token tiles), so
+that they read the scratch after an earlier call left its records there; the outputs start as NaN so that any element a
 call leaves unwritten shows.
 """
 
@@ -19,14 +19,15 @@ from tests.gpu_common import Case, log, require_gpu
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # B, L, H, max_chunks, n_chunks, p, seed: 48 list rows, then 3
-    (2, 1000, 3, 5, 6, 0.4, 3001),
-    (1, 300, 1, 3, 3, 0.6, 3002),
+    # B, L, H, max_chunks, n_chunks, p, seed, tile: 48 list rows, then 3, then 6
+    (2, 1000, 3, 5, 6, 0.4, 3001, 128),
+    (1, 300, 1, 3, 3, 0.6, 3002, 128),
+    (1, 192, 2, 2, 2, 1.0, 3003, 64),
 ]
 
 
-def _prepared(P, B, L, H, mc, n, p, seed):
-    case = Case(P, B, L, H, 128, mc, True, seed)
+def _prepared(P, B, L, H, mc, n, p, seed, T):
+    case = Case(P, B, L, H, T, mc, True, seed)
     for _ in range(n):
         case.append()
     case.gpu_lists(case.rule(p))
@@ -47,7 +48,7 @@ def test_noalloc_backward_matches_the_allocating_entry_point():
         dq = torch.full((case.B, case.L, case.H, 128), float("nan"), dtype=torch.float32, device="cuda")
         dk = torch.full((n_live, case.B, case.L, case.H, 128), float("nan"), dtype=torch.float32, device="cuda")
         dv = torch.full_like(dk, float("nan"))
-        log(f"noalloc bwd B={case.B} L={case.L} H={case.H} rows={case.win.layout.rows}")
+        log(f"noalloc bwd B={case.B} L={case.L} H={case.H} T={case.T} rows={case.win.layout.rows}")
         L.uf_sparse_causal_attn_bwd_noalloc(case.win.handle, q, o, do, lse, case.win.lists, scale, dq, dk, dv)
         got.append((dq, dk, dv))
     torch.cuda.synchronize()
