@@ -7,7 +7,9 @@
 // delta = <dO, O>, dS = P (dO V^T - delta):
 //   dV = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K.
 //
-// Three kernels, all with 32x32x16 bf16 MFMA and fp32 accumulation:
+// Three kernels, all with 32x32x16 bf16 MFMA and fp32 accumulation, each a
+// template on the tile size T (128 or 64; the wave counts below are for 128
+// and halve for 64):
 //  * prep: per query tile, Q and dO rows (rows past the chunk end zero),
 //    -LSE/scale (-inf on those rows, so that their weights vanish) and
 //    -delta, which seed the S and dP accumulators;
