@@ -531,7 +531,7 @@ def main():
     }
     for k in ("split",) if args.split else ():
         line[k] = res[k]
-    for k in ("attn_ms", "attn_ms_p10", "attn_ms_p90", "attn_tflops", "append_us", "append_gbps", "lists_us",
+    for k in ("attn_ms", "attn_ms_median", "attn_ms_p10", "attn_ms_p90", "attn_tflops", "append_us", "append_gbps", "lists_us",
               "topk_budget", "topk_lists_us", "kept_tflop_per_step", "kept_fraction", "padded_tile_tflop_per_step"):
         line[k] = res[k]
     line["roofline"] = {
