@@ -84,15 +84,16 @@ LOGIT_CASES = [
 ]
 
 
+@pytest.mark.parametrize("T", [128, 64])
 @pytest.mark.parametrize("name,q_gain,k_gain", LOGIT_CASES, ids=[c[0] for c in LOGIT_CASES])
-def test_large_and_shifting_logits(name, q_gain, k_gain):
+def test_large_and_shifting_logits(name, q_gain, k_gain, T):
     P = require_gpu()
-    log(f"attn logits case={name}")
+    log(f"attn logits case={name} T={T}")
 
     def gain(chunk, tensor):
         return q_gain if tensor == "q" else (k_gain(chunk) if tensor == "k" else 1.0)
 
-    case = Case(P, 1, 700, 2, 128, 5, True, seed=4242, gain=gain)
+    case = Case(P, 1, 700, 2, T, 5, True, seed=4242, gain=gain)
     for _ in range(5):
         case.append()
     rule = case.rule(0.6)
@@ -230,10 +231,11 @@ def test_stream_head_subset_parity():
 # invariances and degenerate cases
 # ---------------------------------------------------------------------------
 
-def test_eviction_history_gives_bitwise_identical_output():
+@pytest.mark.parametrize("T", [128, 64])
+def test_eviction_history_gives_bitwise_identical_output(T):
     P = require_gpu()
-    a = Case(P, 1, 700, 3, 128, 5, True, seed=42)
-    b = Case(P, 1, 700, 3, 128, 5, True, seed=42)
+    a = Case(P, 1, 700, 3, T, 5, True, seed=42)
+    b = Case(P, 1, 700, 3, T, 5, True, seed=42)
     for _ in range(8):
         a.append()
     for _ in range(4):
@@ -256,11 +258,12 @@ def test_eviction_history_gives_bitwise_identical_output():
     assert torch.equal(oa, oa2) and torch.equal(la, la2)
 
 
-def test_poisoned_padding_never_counts():
+@pytest.mark.parametrize("T", [128, 64])
+def test_poisoned_padding_never_counts(T):
     P = require_gpu()
     outs = []
     for flags in (0, P._lib.UF_F_POISON_PAD):
-        c = Case(P, 1, 300, 2, 128, 3, True, seed=7, flags=flags)
+        c = Case(P, 1, 300, 2, T, 3, True, seed=7, flags=flags)
         for _ in range(4):
             c.append()
         c.gpu_lists(c.rule(0.6))
@@ -268,9 +271,10 @@ def test_poisoned_padding_never_counts():
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
 
 
-def test_v_ones_gives_ones():
+@pytest.mark.parametrize("T", [128, 64])
+def test_v_ones_gives_ones(T):
     P = require_gpu()
-    win = P.KVWindow(1, 2, 300, 128, 3, True)
+    win = P.KVWindow(1, 2, 300, T, 3, True)
     for c in range(3):
         k = synth.custom_tensor((1, 300, 2, 128), 5, c, "k").cuda()
         win.append(k, torch.ones_like(k))
@@ -280,16 +284,19 @@ def test_v_ones_gives_ones():
     assert (o.float() - 1).abs().max().item() <= 1e-2
 
 
-def test_empty_rows_and_stale_entries():
+@pytest.mark.parametrize("T", [128, 64])
+def test_empty_rows_and_stale_entries(T):
     """Rows with no kept tile give O = 0, LSE = -inf; list entries outside the
     window are skipped (hand-made lists, not producible by the builder)."""
     P = require_gpu()
-    case = Case(P, 1, 300, 2, 128, 4, True, seed=3)
+    log(f"attn empty rows + stale entries T={T}")
+    case = Case(P, 1, 300, 2, T, 4, True, seed=3)
     for _ in range(3):
         case.append()
     rule = case.rule(1.0)
     counts, idx, mask = case.gpu_lists(rule)
-    nt, nk = 3, 9
+    nt = -(-300 // T)
+    nk = 3 * nt
     counts = counts.copy()
     idx = idx.copy()
     counts[0, 0, 1] = 0                      # empty row
@@ -302,15 +309,15 @@ def test_empty_rows_and_stale_entries():
     q = case.query()
     o, lse = case.attention(q)
     of, lf = f64(o), f64(lse)
-    assert (of[0, 128:256, 0] == 0).all() and np.isneginf(lf[0, 0, 128:256]).all()
+    assert (of[0, T:2 * T, 0] == 0).all() and np.isneginf(lf[0, 0, T:2 * T]).all()
     bits = np.ones((1, 2, nt, nk), dtype=bool)
     bits[0, 0, 1] = False
     bits[0, 1, 2] = False
     bits[0, 1, 2, [0, 4]] = True
-    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, T, 1 / math.sqrt(128))
     fin = np.isfinite(LSE)
     assert row_rel_err(of[:, :, 1:], O[:, :, 1:]) <= REL_TOL
-    assert np.abs(lf[fin] - LSE[fin]).max() <= lse_tol(128)
+    assert np.abs(lf[fin] - LSE[fin]).max() <= lse_tol(T)
 
 
 def test_lse_optional_and_outputs_untouched_beyond_shape():

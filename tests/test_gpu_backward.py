@@ -233,17 +233,19 @@ def test_backward_full_head_every_tile_and_identities(name):
         assert abs(tv.sum() - to.sum()) <= GRAD_TOL * (np.abs(tv).sum() + np.abs(to).sum())
 
 
-def test_backward_empty_rows_and_stale_entries():
+@pytest.mark.parametrize("T", [128, 64])
+def test_backward_empty_rows_and_stale_entries(T):
     """A row with no kept tile gets zero gradients and gives none; a list entry
     outside the window counts no key (hand-made lists, index and mask sections
     kept consistent)."""
     P = require_gpu()
-    log("bwd empty rows + stale entries")
-    case = Case(P, 1, 300, 2, 128, 4, True, seed=2103)
+    log(f"bwd empty rows + stale entries T={T}")
+    case = Case(P, 1, 300, 2, T, 4, True, seed=2103)
     for _ in range(3):
         case.append()
     counts, idx, mask = case.gpu_lists(case.rule(1.0))
-    nt, nk = 3, 9
+    nt = -(-300 // T)
+    nk = 3 * nt
     counts, idx, mask = counts.copy(), idx.copy(), mask.copy()
     counts[0, 0, 1] = 0                          # empty row
     idx[0, 0, 1, :] = -1
@@ -267,7 +269,7 @@ def test_backward_empty_rows_and_stale_entries():
     bits[0, 0, 1] = False
     bits[0, 1, 2] = False
     bits[0, 1, 2, [0, 4]] = True
-    rq, rk, rv = oracle.sparse_causal_attention_bwd(case.ring, case._host(q), case._host(do), bits, 128, scale)
+    rq, rk, rv = oracle.sparse_causal_attention_bwd(case.ring, case._host(q), case._host(do), bits, T, scale)
     gq, gk, gv = dq.cpu().numpy(), dk.cpu().numpy(), dv.cpu().numpy()
-    assert np.all(gq[0, 128:256, 0] == 0)
+    assert np.all(gq[0, T:2 * T, 0] == 0)
     _compare_heads(gq, gk, gv, rq, rk, rv, [(0, 0), (1, 1)], 1)
