@@ -55,6 +55,10 @@ SMALL = [
     (1, 100, 2, 128, 1, False, 1, 0.0),
     # ... or the pinned tile and the current one (four units)
     (2, 100, 2, 128, 2, True, 2, 1.0),
+    # 64-token tiles with long lists (up to 188 tiles per row) and with more
+    # rows (320) than compute units
+    (1, 3000, 3, 64, 4, True, 5, 0.4),
+    (2, 2500, 4, 64, 3, False, 3, 1.0),
 ]
 
 
