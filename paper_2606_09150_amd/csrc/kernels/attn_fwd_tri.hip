@@ -331,10 +331,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
       qf[ks] = as_bf16x8(u);
     }
   }
-  // Q is in registers before any page copy is issued, so that the only
-  // vector-memory operations in flight inside the loop are page copies.
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
-
   // Operand read offsets (16-key or 16-dim step j, row ln of a 32-row block)
   // and the lane's copy source offset (copies c with c % 2 == qw % 2).
   uint32_t rd[4];
@@ -357,31 +353,44 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_tri_kernel(AttnArgs a) {
   if constexpr (UNITS) {
     // non-empty units of the row's slice, in list order; entries naming a
     // tile outside the window count no key and give none
+    // (the list entries of four 64-entry groups are requested together, and
+    // their latency overlaps that of the Q loads above)
     if (wave == 0) {
       const int32_t* lv = a.idx + size_t(row) * a.nk_cap + first;
       int off = 0;
-      for (int base = 0; base < count; base += 64) {
-        const int e = base + lane;
-        int n = 0;
-        uint32_t j = 0;
-        if (e < count) {
-          j = uint32_t(lv[e]);
+      for (int base = 0; base < count; base += 256) {
+        uint32_t jj[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int e = base + 64 * k + lane;
+          jj[k] = e < count ? uint32_t(lv[e]) : 0xffffffffu;
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t j = jj[k];
+          int n = 0;
           if (j < uint32_t(a.nk)) {
             const int v = tile_valid(a.tv, int(j % uint32_t(a.NT)), a.NT, a.tail, kT);
             n = (v > 64) ? 2 : (v > 0 ? 1 : 0);
           }
+          const uint64_t b1 = __ballot(n >= 1), b2 = __ballot(n == 2);
+          const uint64_t below = (uint64_t(1) << lane) - 1;
+          const int pos = off + __popcll(b1 & below) + __popcll(b2 & below);
+          if (n >= 1) sunit[pos] = j << 1;
+          if (n == 2) sunit[pos + 1] = (j << 1) | 1u;
+          off += __popcll(b1) + __popcll(b2);
         }
-        const uint64_t b1 = __ballot(n >= 1), b2 = __ballot(n == 2);
-        const uint64_t below = (uint64_t(1) << lane) - 1;
-        const int pos = off + __popcll(b1 & below) + __popcll(b2 & below);
-        if (n >= 1) sunit[pos] = j << 1;
-        if (n == 2) sunit[pos + 1] = (j << 1) | 1u;
-        off += __popcll(b1) + __popcll(b2);
       }
       if (lane == 0) sunit[kUnitCap] = uint32_t(off);
     }
+    // Q and the list entries are in registers before any page copy is
+    // issued, so that the only vector-memory operations in flight inside the
+    // loop are page copies.
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
     U = int(__builtin_amdgcn_readfirstlane(sunit[kUnitCap]));
+  } else {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   }
   const int P = U + 3;                // phases
 
