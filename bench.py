@@ -108,7 +108,7 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(total)]
     work = None
     n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
-    if split == "tail":
+    if split == "tail" or isinstance(split, tuple):
         pass   # sized in the first (warm-up) step, once the window is full: the plan depends on its length
     elif split:
         work = torch.empty(P.uf_attn_split_work_bytes(win.handle, split), dtype=torch.uint8, device=dev)
@@ -126,8 +126,9 @@ def run_workload(P, wl, steps, warmup, n_src=3, split=0):
         win.lists = lists[s]
         win.build_lists(wl.seed, wl.p_prior)
         nonlocal work
-        if split == "tail" and work is None:
-            need = P.uf_attn_split_rows_work_bytes(win.handle, *P.uf_attn_tail_plan(win.handle, n_cu))
+        if (split == "tail" or isinstance(split, tuple)) and work is None:
+            rows = P.uf_attn_tail_plan(win.handle, n_cu) if split == "tail" else split
+            need = P.uf_attn_split_rows_work_bytes(win.handle, *rows)
             work = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
         e[2].record(stream)
         win.attention(src["q"], scale, out=out, lse=lse, split=split, work=work)
@@ -578,6 +579,13 @@ def main():
                 others[name]["tail_split"] = {k: r[k] for k in ("ms_per_step", "attn_ms", "attn_ms_median",
                                                                 "attn_tflops")}
                 others[name]["tail_split"]["roofline_frac"] = r["attn_tflops"] / MFMA_BF16_PEAK_TFLOPS
+                n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+                others[name]["tail_split"]["plan"] = list(P.uf_attn_tail_plan(st2["win"].handle, n_cu))
+                del st2
+                # and rows 256.. (the last round on 256 CUs) in 4 slices, whether or not the plan takes it
+                r, st2 = run_workload(P, synth.WORKLOADS[name], 10, args.warmup, split=(256, 4))
+                others[name]["split_rows_256_4"] = {k: r[k] for k in ("ms_per_step", "attn_ms", "attn_ms_median",
+                                                                      "attn_tflops")}
                 del st2
         others["1k_stream"] = run_stream(P, synth.WORKLOADS["1k_stream"])
         line["others"] = others

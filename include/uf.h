@@ -320,11 +320,11 @@ int uf_sparse_causal_attn_fwd_split(const uf_kv* kv, const void* d_q, const void
  * tile size): split_from = C * floor(R / C) and the n_split in 2..8
  * (in 2..min(64, C / R) when R < C), at most the window's key tiles, that
  * makes the last round shortest, in row-times
- * ceil((R - split_from) * n_split / C) / n_split; it returns split_from = R
- * and n_split = 1 (no split) when R is a multiple of C or when the saving is
- * under a fifth of a row-time or under 16 key tiles of one row's work (the
- * window's key tiles times the saved row-time: short rows do not repay the
- * merge launch).  Results equal those of uf_sparse_causal_attn_fwd
+ * ceil((R - split_from) * n_split / C) * (1 / n_split + 9 / nk) + 12 / nk
+ * (nk = the window's key tiles: a slice's fixed cost and the merge launch,
+ * measured, in key tiles of work); it returns split_from = R and
+ * n_split = 1 (no split) when R is a multiple of C or when the saving is
+ * under a fifth of a row-time or under 16 key tiles of one row's work.  Results equal those of uf_sparse_causal_attn_fwd
  * up to float rounding order.  Errors: UF_ERR_ARG, UF_ERR_EMPTY, UF_ERR_HIP. */
 int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_t* n_split);
 int uf_attn_split_rows_work_bytes(const uf_kv* kv, int32_t split_from, int32_t n_split, size_t* bytes);

@@ -479,8 +479,12 @@ int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_
   *split_from = int32_t(R);
   *n_split = 1;
   // time in row-times with rounds of C workgroups: whole rows take
-  // ceil(R / C); rows F.. cut into S slices take
-  // F / C + ceil((R - F) * S / C) / S with F = C * floor(R / C)
+  // ceil(R / C); rows F.. cut into S slices take F / C + ceil((R - F) * S / C)
+  // rounds of 1/S row-time plus a slice's fixed cost, and the merge launch
+  // follows (F = C * floor(R / C)).  The fixed costs, in key tiles of work
+  // (a row of the window is taken as dense, nk tiles), are measured ones: a
+  // slice's prologue and epilogue about 9 tiles, the merge about 12.
+  constexpr double kSliceTiles = 9.0, kMergeTiles = 12.0;
   const int64_t q = R / C, r = R % C;
   if (r == 0) return ok();
   const double whole = double(q + 1);
@@ -490,7 +494,8 @@ int uf_attn_tail_plan(const uf_kv* kv, int32_t n_cu, int32_t* split_from, int32_
   double best = whole;
   int32_t best_s = 1;
   for (int64_t S = 2; S <= s_max; ++S) {
-    const double cost = double(q) + double((r * S + C - 1) / C) / double(S);
+    const double cost = double(q) + double((r * S + C - 1) / C) * (1.0 / double(S) + kSliceTiles / double(nk)) +
+                        kMergeTiles / double(nk);
     if (cost < best - 1e-9) {
       best = cost;
       best_s = int32_t(S);

@@ -126,8 +126,9 @@ class KVWindow:
 
         ``split`` > 0 selects split-KV attention with that many list slices per
         row; ``split="tail"`` splits only the rows of the last, partly filled
-        round of one workgroup per compute unit (uf_attn_tail_plan); ``work``
-        is the scratch buffer of either (allocated here when None)."""
+        round of one workgroup per compute unit as uf_attn_tail_plan chooses,
+        and ``split=(split_from, n_split)`` rows split_from.. into n_split
+        slices; ``work`` is the scratch buffer (allocated here when None)."""
         _check_chunk(q, "q", self.B, self.L, self.H, self.D)
         if scale is None:
             scale = 1.0 / math.sqrt(self.D)
@@ -145,9 +146,12 @@ class KVWindow:
         buf = self.lists if lists is None else lists
         if buf.numel() < self.layout.total_bytes:
             raise ValueError("list buffer too small")
-        if split == "tail":
-            n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
-            split_from, n_split = L.uf_attn_tail_plan(self.handle, n_cu)
+        if split == "tail" or isinstance(split, tuple):
+            if split == "tail":
+                n_cu = torch.cuda.get_device_properties(q.device).multi_processor_count
+                split_from, n_split = L.uf_attn_tail_plan(self.handle, n_cu)
+            else:
+                split_from, n_split = (int(x) for x in split)
             need = L.uf_attn_split_rows_work_bytes(self.handle, split_from, n_split)
             if work is None and need > 0:
                 work = torch.empty(need, dtype=torch.uint8, device=q.device)

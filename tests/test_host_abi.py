@@ -315,8 +315,10 @@ def test_tail_plan_and_split_rows_host_paths(P):
             w.append(None, None)
         return L.uf_attn_tail_plan(w.handle, n_cu)
 
-    # 480p: 444 rows on 256 CUs -> rows 256.. in 4 slices (1.75 row-times instead of 2)
-    assert plan(1, 4680, 12, 256, chunks=4) == (256, 4)
+    # 480p: 444 rows on 256 CUs; 4 slices of rows 256.. would take 1.75
+    # row-times plus three slices' and the merge's fixed costs (2.03 against
+    # 2 whole), so no split
+    assert plan(1, 4680, 12, 256, chunks=4) == (444, 1)
     # 1K: 2,304 rows are nine whole rounds; 2K: 4,056 rows leave 216 in the last
     # round, where no slice count saves a fifth of a row-time
     assert plan(1, 24480, 12, 256, chunks=5) == (2304, 1)
