@@ -507,3 +507,29 @@ def test_tiny_workload_split_rows():
     lerr = float(np.abs(f64(lse) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL and lerr <= lse_tol(64)
+
+
+def test_plan_chosen_split_long_window_few_rows():
+    """A window of 32 chunks whose 5 rows (one head, 5 query tiles) fill few
+    CUs: the plan cuts every row into 51 slices, and the attention with
+    split="tail" (plan, split launch, merge) matches the oracle in full."""
+    P = require_gpu()
+    L = P._lib
+    log("attn plan-chosen split: 32 chunks, 5 rows")
+    case = Case(P, 1, 640, 1, 128, 32, True, seed=83)
+    for _ in range(32):
+        case.append()
+    assert L.uf_attn_tail_plan(case.win.handle, 256) == (0, 51)
+    rule = case.rule(0.6)
+    case.gpu_lists(rule)
+    q = case.query()
+    o, lse = case.win.attention(q, split="tail")
+    o1, l1 = case.win.attention(q)
+    torch.cuda.synchronize()
+    bits = case.oracle_bits(rule)
+    O, LSE = oracle.sparse_causal_attention(case.ring, case._host(q), bits, 128, 1 / math.sqrt(128))
+    err = row_rel_err(case._host(o), O)
+    lerr = float(np.abs(f64(lse) - LSE).max())
+    log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
+    assert err <= REL_TOL and lerr <= lse_tol(128)
+    assert row_rel_err(case._host(o), case._host(o1)) <= REL_TOL
