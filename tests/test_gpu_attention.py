@@ -429,6 +429,10 @@ def test_split_rows_parity_and_plan():
     lerr = float(np.abs(f64(lse) - LSE).max())
     log(f"  rel_err={err:.3e} lse_err={lerr:.3e}")
     assert err <= REL_TOL and lerr <= lse_tol(128)
+    # the binding's split=(split_from, n_split) is the same call
+    o2, l2 = case.win.attention(q, 1 / math.sqrt(128), split=(20, 3))
+    torch.cuda.synchronize()
+    assert torch.equal(o2, o) and torch.equal(l2, lse)
     # rows before split_from run the unsplit code: bit-identical to the plain kernel
     rows_whole = 20                  # rows (b*H + h)*NT + i with NT = 6
     for r in range(rows_whole):
